@@ -1,0 +1,165 @@
+/*
+ * grinqh.h -- C ABI of libgrinqh, the nested-precision decode VMM of GRINQH
+ * (Graded Input-based Quantization Hierarchy, arXiv 2606.23419) for AMD
+ * Instinct MI355X (gfx950).
+ *
+ * The path (Sec. 3 of the paper):
+ *   offline   W (fp16) --RTN, 8 bits, group 128--> codes + scales
+ *             codes --nest + pack--> bit planes, most significant first
+ *   per token x --magnitude grading--> a level per input channel
+ *             y = W_hat(levels) x, each weight row read only to the depth its
+ *             channel's level asks for (Sec. 3.3 "Storage Layout and Weight
+ *             Loading"; App. C.1 "Sparse bit-loading").
+ *
+ * Conventions for every entry point
+ *   - Device pointers are plain HIP device addresses owned by the caller; the
+ *     library never allocates, frees or synchronises.  Host pointers are read
+ *     during the call only.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *     All work is enqueued on it; nothing waits for it.
+ *   - Every argument is validated on the host before anything is enqueued; a
+ *     failing call returns a negative status, writes nothing and leaves a
+ *     message for grinqh_last_error().  A failing launch returns GRINQH_EHIP.
+ *     Faults inside kernels surface at the caller's next synchronisation.
+ *   - Calls are thread-safe; the error message is per thread.
+ *
+ * Packed layout (the contract between grinqh_pack and grinqh_vmm)
+ *   u (plane_bits) in {1, 2}; P = 8/u planes; T (tile_n) outputs per tile.
+ *   codes buffer: (N/T) tiles x K rows x T bytes = K*N bytes.
+ *   Row (tile t, channel k) starts at byte (t*K + k)*T.  Plane j (1-based,
+ *   j = 1 most significant) starts at byte (j-1)*T*u/8 of the row and holds,
+ *   for local output o = n - t*T, the field (q >> (8 - j*u)) & (2^u - 1) at
+ *   bit o*u of the plane (byte floor(o*u/8), bit (o*u) % 8, little-endian).
+ *   Reading b bits of a channel therefore reads the first b*T/8 bytes of its
+ *   row in every tile: a contiguous prefix, a multiple of 64 bytes.
+ *   scales buffer: fp16 [K/128][N], the scale of group g for output n at
+ *   index g*N + n.  Codes are offset binary: w_hat = s*(q - 128) at 8 bits.
+ */
+#ifndef GRINQH_H
+#define GRINQH_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#if defined(__GNUC__)
+#define GRINQH_API __attribute__((visibility("default")))
+#else
+#define GRINQH_API
+#endif
+
+typedef enum {
+  GRINQH_OK = 0,
+  GRINQH_EINVAL = -1,       /* invalid argument: null pointer, bad shape, bad ordering */
+  GRINQH_EUNSUPPORTED = -2, /* well-formed but outside what these kernels implement */
+  GRINQH_ESIZE = -3,        /* workspace too small, or a size overflows */
+  GRINQH_EHIP = -4          /* the HIP runtime reported an error at launch */
+} grinqh_status;
+
+#define GRINQH_MAX_LEVELS 9
+
+/* Layer descriptor: 36 bytes, natural alignment, no implicit padding. */
+typedef struct {
+  int32_t K;          /* input channels (d_in); a multiple of `group` */
+  int32_t N;          /* outputs (d_out); a multiple of the tile width */
+  int32_t group;      /* quantisation group along K; must be 128 */
+  int32_t n_levels;   /* number of levels n+1 including level 0; 2..9 */
+  uint8_t level_bits[GRINQH_MAX_LEVELS];
+                      /* b_0 = 0 < b_1 < ... < b_n = 8 (Sec. 3.1: the set B);
+                         every b_i a multiple of plane_bits */
+  uint8_t reserved_[3];
+  int32_t plane_bits; /* u: 0 = auto (2 if every b_i is even, else 1); or 1, 2 */
+  int32_t tile_n;     /* T: 0 = auto; else 256, 512, 1024 or 2048 with T*u >= 512 */
+} grinqh_layer_desc;
+
+enum { GRINQH_SRC_FP16_RTN = 0, GRINQH_SRC_CODES_U8 = 1 };
+enum { GRINQH_ASSIGN_THRESHOLD = 0, GRINQH_ASSIGN_TOPK = 1 };
+enum { GRINQH_VMM_ACCUMULATE = 1 };
+
+/* Fill the auto fields (plane_bits, tile_n) of *in into *out after
+ * validating it.  Host only.  Every other entry point resolves the same way. */
+GRINQH_API int grinqh_resolve_desc(const grinqh_layer_desc* in, grinqh_layer_desc* out);
+
+/* Sizes of the packed buffers of a layer (host only): codes K*N bytes,
+ * scales 2*(K/128)*N bytes. */
+GRINQH_API int grinqh_packed_bytes(const grinqh_layer_desc* desc, size_t* codes_bytes,
+                        size_t* scales_bytes);
+
+/* Offline quantise + nest + pack (Sec. 3.3, App. C.1).
+ *   src_kind GRINQH_SRC_FP16_RTN: src = fp16 W[N][K] (torch Linear.weight
+ *     layout), src_scales = NULL.  Symmetric RTN per (output, group of 128
+ *     channels): s = fp16_rne(fp32(max|w|)/127), q = clamp(rne(w/s), -128, 127)
+ *     + 128; a group with s == 0 gets q = 128.  W must be finite.
+ *   src_kind GRINQH_SRC_CODES_U8: src = uint8 codes q[N][K] from any base
+ *     quantiser with the same offset-binary convention, src_scales = fp16
+ *     s[N][K/128] (the method is quantisation-agnostic, Sec. 3.3).
+ *   Outputs: packed_codes (K*N bytes, layout above), packed_scales
+ *   (fp16 [K/128][N]).  Inputs and outputs must not overlap. */
+GRINQH_API int grinqh_pack(const grinqh_layer_desc* desc, int src_kind, const void* src,
+                const void* src_scales, void* packed_codes, void* packed_scales,
+                void* stream);
+
+/* Integer channel counts for a precision distribution P given in basis
+ * points (p_0..p_n, each >= 0, summing to 10000; App. A.1).  With
+ * U_j = sum_{i>=j} p_i, C_j = floor((U_j*K + 5000)/10000) channels get level
+ * >= j; counts_out[j] = C_j - C_{j+1} (n+1 values summing to K).  Host only. */
+GRINQH_API int grinqh_topk_counts(int32_t K, int32_t n_levels, const int32_t* p_bp,
+                       int32_t* counts_out);
+
+/* Device workspace needed by grinqh_assign / grinqh_vmm for B tokens.  The
+ * present kernels need none and report 0; callers may pass NULL/0. */
+GRINQH_API int grinqh_workspace_bytes(const grinqh_layer_desc* desc, int32_t B, size_t* bytes);
+
+/* Per-token precision assignment (Sec. 3.1; App. A.1).
+ *   x: fp16 [B][K] (device), finite.
+ *   mode GRINQH_ASSIGN_THRESHOLD: thresholds = host fp32 theta_1..theta_n
+ *     (n = n_levels-1), non-decreasing, not NaN (+inf allowed); channel k gets
+ *     the level l with |x_k| in [theta_l, theta_{l+1}), theta_0 = 0,
+ *     theta_{n+1} = +inf, |x| compared in fp32.  counts = NULL.
+ *   mode GRINQH_ASSIGN_TOPK: counts = host int32 c_0..c_n summing to K (e.g.
+ *     from grinqh_topk_counts).  Channels are ordered by |x| descending, ties
+ *     by lower index; the first c_n get level n, the next c_{n-1} level n-1,
+ *     and so on.  thresholds = NULL.  Requires K <= 65536.
+ *   level_map: uint8 [B][K] (device), the level index per channel. */
+GRINQH_API int grinqh_assign(const grinqh_layer_desc* desc, int mode, const void* x, int32_t B,
+                  const float* thresholds, const int32_t* counts, uint8_t* level_map,
+                  void* workspace, size_t ws_bytes, void* stream);
+
+/* Nested-precision decode VMM (Sec. 3.3 reconstruction; App. C.1).
+ *   y[t][n] = sum_k x[t][k] * w_hat(k, n), with w_hat = s*(q_b*2^(8-b) + phi
+ *   - 128) for the b = level_bits[level_map[t][k]] most significant bits q_b
+ *   of the code, phi = 2^(7-b) for 0 < b < 8, phi = 0 at b = 8, and channels
+ *   at level 0 skipped.  Only the first b*T/8 bytes of each of a channel's
+ *   rows are read; for B > 1 the deepest level over the B tokens is read once
+ *   and each token uses its own prefix of it.
+ *   x: fp16 [B][K]; level_map: uint8 [B][K], values < n_levels (a larger
+ *   value is read as the top level); y: fp32 [B][N]; 1 <= B <= 4.
+ *   flags: 0 -> y is overwritten; GRINQH_VMM_ACCUMULATE -> y += result (the
+ *   caller initialised y).  Accumulation order across K is not fixed, so y
+ *   is reproducible to rounding, not bit for bit. */
+GRINQH_API int grinqh_vmm(const grinqh_layer_desc* desc, const void* packed_codes,
+               const void* packed_scales, const void* x, const uint8_t* level_map,
+               int32_t B, float* y, int32_t flags, void* workspace, size_t ws_bytes,
+               void* stream);
+
+/* The VMM with the threshold assignment of Sec. 3.1 fused into it: each
+ * channel's level is graded inside the kernel from |x| and `thresholds`
+ * (host fp32 theta_1..theta_n, rules as in grinqh_assign), so no level map
+ * is read; if level_map_out is not NULL the levels are also written there
+ * (uint8 [B][K]).  Other arguments as grinqh_vmm. */
+GRINQH_API int grinqh_vmm_threshold(const grinqh_layer_desc* desc, const void* packed_codes,
+                         const void* packed_scales, const void* x, int32_t B,
+                         const float* thresholds, uint8_t* level_map_out, float* y,
+                         int32_t flags, void* workspace, size_t ws_bytes, void* stream);
+
+/* Message of the last failing call on this thread ("" if none). */
+GRINQH_API const char* grinqh_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GRINQH_H */

@@ -1,0 +1,61 @@
+// Internal definitions shared by the libgrinqh translation units.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "../../include/grinqh.h"
+
+namespace grinqh {
+
+constexpr int kGroup = 128;       // quantisation group along K
+constexpr int kMaxLevels = GRINQH_MAX_LEVELS;
+constexpr int kMaxB = 4;          // tokens per VMM call
+
+// A validated, resolved layer descriptor, passed to kernels by value.
+struct Layer {
+  int K, N, n_levels;
+  int u;            // plane width in bits (1 or 2)
+  int P;            // number of planes, 8/u
+  int T;            // outputs per tile
+  int tiles;        // N / T
+  int groups;       // K / 128
+  int bits[kMaxLevels];    // b_l
+  int planes[kMaxLevels];  // b_l / u: planes read at level l
+};
+
+struct Thresholds {
+  float theta[kMaxLevels - 1];   // theta_1 .. theta_n
+  int n;
+};
+
+struct TopkCuts {
+  int cum[kMaxLevels];           // cum[j] = C_{j+1}: channels at level >= j+1
+  int n;
+};
+
+// fp16 <-> fp32 helpers on raw bits.
+__device__ __forceinline__ float h2f(uint16_t b) {
+  return (float)__builtin_bit_cast(_Float16, b);
+}
+__device__ __forceinline__ uint16_t f2h_rn(float f) {
+  return __builtin_bit_cast(uint16_t, (_Float16)f);
+}
+
+// Error reporting (per thread), defined in grinqh_api.hip.
+int fail(int status, const char* fmt, ...);
+int check_launch(const char* what);
+
+// Kernel launchers (defined next to their kernels).
+int launch_pack(const Layer& L, int src_kind, const void* src, const void* src_scales,
+                void* packed_codes, void* packed_scales, hipStream_t s);
+int launch_assign_threshold(const Layer& L, const void* x, int B, const Thresholds& th,
+                            uint8_t* level_map, hipStream_t s);
+int launch_assign_topk(const Layer& L, const void* x, int B, const TopkCuts& cuts,
+                       uint8_t* level_map, hipStream_t s);
+int launch_vmm(const Layer& L, const void* codes, const void* scales, const void* x,
+               const uint8_t* level_map, const Thresholds* th, uint8_t* level_map_out,
+               int B, float* y, int accumulate, hipStream_t s);
+
+}  // namespace grinqh

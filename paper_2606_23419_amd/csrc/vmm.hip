@@ -1,0 +1,133 @@
+// Nested-precision decode VMM (Sec. 3.3 reconstruction with the midpoint
+// bias; App. C.1 sparse bit-loading), first version: correctness first.
+//
+// Grid: (tiles x K-splits, tokens).  A workgroup owns one tile of T outputs
+// and a range of whole groups.  Its 256 threads form lane groups of T/16
+// lanes; each lane holds 16 consecutive outputs of the tile.  Lane group lg
+// takes the rows lg, lg + nlg, ... of every group, reads the first
+// planes[level] planes of each row (a contiguous prefix), rebuilds the
+// truncated code t = q_b << (8 - b) and accumulates x_k * t.  Per group,
+//   y_n += s_{g,n} * (sum_k x_k t_{k,n} + beta_g),
+//   beta_g = sum_{k in g, level > 0} x_k (phi_b - 128),
+// which is sum_k x_k * s * (t + phi - 128) with the scale factored out.
+// Lane groups are reduced through LDS and added into y with atomics.
+#include "grinqh_internal.h"
+
+namespace grinqh {
+
+constexpr int kVmmThreads = 256;
+
+__device__ __forceinline__ float midpoint_minus_offset(int b) {
+  // phi_b - 128 with phi_b = 2^(7-b) for 0 < b < 8 and phi_8 = 0
+  return (b < 8 ? (float)(1 << (7 - b)) : 0.0f) - 128.0f;
+}
+
+__global__ __launch_bounds__(256) void k_zero(float* __restrict__ y, long n) {
+  const long i = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) y[i] = 0.0f;
+}
+
+template <int U>
+__global__ __launch_bounds__(kVmmThreads) void k_vmm_v0(
+    const uint8_t* __restrict__ codes, const uint16_t* __restrict__ scales,
+    const uint16_t* __restrict__ x, const uint8_t* __restrict__ lm, float* __restrict__ y,
+    Layer L, int groups_per_split, int fused, Thresholds th, uint8_t* __restrict__ lm_out) {
+  constexpr uint32_t MASK = (1u << U) - 1u;
+  __shared__ float red[kVmmThreads * 16];
+
+  const int t = blockIdx.x % L.tiles;
+  const int split = blockIdx.x / L.tiles;
+  const int tok = blockIdx.y;
+  const int lanes = L.T / 16;
+  const int nlg = kVmmThreads / lanes;
+  const int lg = threadIdx.x / lanes, li = threadIdx.x % lanes;
+  const int g0 = split * groups_per_split;
+  const int g1 = min(g0 + groups_per_split, L.groups);
+  const uint16_t* xt = x + (size_t)tok * L.K;
+  const int plane_bytes = L.T * U / 8;
+
+  float yacc[16];
+#pragma unroll
+  for (int e = 0; e < 16; ++e) yacc[e] = 0.0f;
+
+  for (int g = g0; g < g1; ++g) {
+    float acc[16];
+#pragma unroll
+    for (int e = 0; e < 16; ++e) acc[e] = 0.0f;
+    float beta = 0.0f;
+    for (int r = lg; r < kGroup; r += nlg) {
+      const int k = g * kGroup + r;
+      const float xv = h2f(xt[k]);
+      int lvl;
+      if (fused) {
+        const float a = fabsf(xv);
+        lvl = 0;
+        for (int j = 0; j < th.n; ++j) lvl += a >= th.theta[j] ? 1 : 0;
+        if (lm_out && t == 0 && li == 0) lm_out[(size_t)tok * L.K + k] = (uint8_t)lvl;
+      } else {
+        lvl = min((int)lm[(size_t)tok * L.K + k], L.n_levels - 1);
+      }
+      if (lvl == 0) continue;
+      const int d = L.planes[lvl];
+      const int b = d * U;
+      const uint8_t* row = codes + ((size_t)t * L.K + k) * L.T;
+      uint32_t code[16];
+#pragma unroll
+      for (int e = 0; e < 16; ++e) code[e] = 0u;
+      for (int j = 0; j < d; ++j) {
+        uint32_t word;
+        if (U == 2) word = *(const uint32_t*)(row + (size_t)j * plane_bytes + li * 4);
+        else word = *(const uint16_t*)(row + (size_t)j * plane_bytes + li * 2);
+#pragma unroll
+        for (int e = 0; e < 16; ++e) code[e] = (code[e] << U) | ((word >> (e * U)) & MASK);
+      }
+      const int sh = 8 - b;
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[e] = fmaf(xv, (float)(code[e] << sh), acc[e]);
+      beta = fmaf(xv, midpoint_minus_offset(b), beta);
+    }
+    const uint16_t* sg = scales + (size_t)g * L.N + (size_t)t * L.T + li * 16;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) yacc[e] = fmaf(h2f(sg[e]), acc[e] + beta, yacc[e]);
+  }
+
+#pragma unroll
+  for (int e = 0; e < 16; ++e) red[lg * L.T + li * 16 + e] = yacc[e];
+  __syncthreads();
+  float* yt = y + (size_t)tok * L.N + (size_t)t * L.T;
+  for (int o = threadIdx.x; o < L.T; o += kVmmThreads) {
+    float s = 0.0f;
+    for (int q = 0; q < nlg; ++q) s += red[q * L.T + o];
+    atomicAdd(&yt[o], s);
+  }
+}
+
+int launch_vmm(const Layer& L, const void* codes, const void* scales, const void* x,
+               const uint8_t* level_map, const Thresholds* th, uint8_t* level_map_out,
+               int B, float* y, int accumulate, hipStream_t s) {
+  if (!accumulate) {
+    const long n = (long)B * L.N;
+    hipLaunchKernelGGL(k_zero, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, y, n);
+    int st = check_launch("vmm zero-fill");
+    if (st) return st;
+  }
+  // about 512 workgroups per token over the whole chip
+  int ksplit = (512 + L.tiles - 1) / L.tiles;
+  if (ksplit > L.groups) ksplit = L.groups;
+  const int gps = (L.groups + ksplit - 1) / ksplit;
+  ksplit = (L.groups + gps - 1) / gps;
+  const dim3 grid((unsigned)(L.tiles * ksplit), (unsigned)B);
+  Thresholds none{};
+  const int fused = th != nullptr;
+  if (L.u == 2)
+    hipLaunchKernelGGL(k_vmm_v0<2>, grid, dim3(kVmmThreads), 0, s, (const uint8_t*)codes,
+                       (const uint16_t*)scales, (const uint16_t*)x, level_map, y, L, gps, fused,
+                       fused ? *th : none, level_map_out);
+  else
+    hipLaunchKernelGGL(k_vmm_v0<1>, grid, dim3(kVmmThreads), 0, s, (const uint8_t*)codes,
+                       (const uint16_t*)scales, (const uint16_t*)x, level_map, y, L, gps, fused,
+                       fused ? *th : none, level_map_out);
+  return check_launch("vmm");
+}
+
+}  // namespace grinqh

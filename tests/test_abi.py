@@ -1,0 +1,155 @@
+"""C-ABI checks that need no GPU: the library loads, exports every declared
+symbol, and its host-side validation rejects bad arguments before enqueuing
+anything.  Every device entry point called here is given arguments that fail
+validation, so no kernel is ever launched from this file."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from oracle import grinqh_oracle as orc
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def g():
+    from paper_2606_23419_amd import grinqh
+    return grinqh
+
+
+def test_library_exports_every_declared_symbol(g):
+    hdr = open(os.path.join(ROOT, "include", "grinqh.h")).read()
+    declared = set(re.findall(r"GRINQH_API\s+[\w\s\*]+?\b(grinqh_\w+)\s*\(", hdr))
+    assert declared == set(g.EXPORTED)
+    for name in declared:
+        assert hasattr(g.lib, name), name
+
+
+def test_desc_struct_layout_matches_header(g):
+    assert ctypes.sizeof(g.LayerDesc) == 36
+    assert g.LayerDesc.level_bits.offset == 16
+    assert g.LayerDesc.plane_bits.offset == 28
+    assert g.LayerDesc.tile_n.offset == 32
+
+
+def test_resolve_auto_fields(g):
+    r = g.grinqh_resolve_desc(g.make_desc(4096, 4096, (0, 2, 4, 6, 8)))
+    assert (r.plane_bits, r.tile_n) == (2, 512)
+    r = g.grinqh_resolve_desc(g.make_desc(4096, 6144, (0, 2, 3, 4, 8)))
+    assert (r.plane_bits, r.tile_n) == (1, 512)
+    r = g.grinqh_resolve_desc(g.make_desc(1024, 1024, (0, 2, 4, 8), tile_n=256))
+    assert (r.plane_bits, r.tile_n) == (2, 256)
+    # N = 768 is a multiple of 256 only
+    r = g.grinqh_resolve_desc(g.make_desc(128, 768, (0, 2, 4, 8)))
+    assert r.tile_n == 256
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(K=0, N=512, level_bits=(0, 8)), -1),
+    (dict(K=100, N=512, level_bits=(0, 8)), -1),
+    (dict(K=128, N=512, level_bits=(0, 8), group=64), -2),
+    (dict(K=128, N=512, level_bits=(2, 8)), -1),
+    (dict(K=128, N=512, level_bits=(0, 4, 6)), -1),
+    (dict(K=128, N=512, level_bits=(0, 4, 4, 8)), -1),
+    (dict(K=128, N=512, level_bits=(0,)), -1),
+    (dict(K=128, N=512, level_bits=(0, 3, 8), plane_bits=2), -1),
+    (dict(K=128, N=512, level_bits=(0, 8), plane_bits=4), -2),
+    (dict(K=128, N=512, level_bits=(0, 8), tile_n=384), -2),
+    (dict(K=128, N=512, level_bits=(0, 3, 8), tile_n=256), -2),
+    (dict(K=128, N=768, level_bits=(0, 8), tile_n=512), -1),
+    (dict(K=128, N=100, level_bits=(0, 8)), -2),
+])
+def test_resolve_rejects(g, kw, status):
+    d = g.make_desc(**kw)
+    with pytest.raises(g.GrinqhError) as e:
+        g.grinqh_resolve_desc(d)
+    assert e.value.status == status
+    assert g.grinqh_last_error()
+
+
+def test_packed_bytes_and_workspace(g):
+    d = g.make_desc(4096, 14336, (0, 2, 4, 6, 8))
+    assert g.grinqh_packed_bytes(d) == (4096 * 14336, 32 * 14336 * 2)
+    assert g.grinqh_workspace_bytes(d, 4) == 0
+
+
+@pytest.mark.parametrize("K", [1, 7, 128, 1024, 4096, 14336])
+def test_topk_counts_match_oracle(g, K):
+    for p in [(3000, 5000, 1500, 500), (2500, 2200, 3100, 2200, 0), (2000, 1000, 2000, 2000, 3000),
+              (0, 0, 0, 10000), (3333, 3333, 3334)]:
+        assert g.grinqh_topk_counts(K, p) == orc.topk_counts(K, p).tolist()
+
+
+def test_topk_counts_rejects(g):
+    for K, p in [(0, (5000, 5000)), (16, (5000, 4000)), (16, (-1, 10001)), (16, (10000,))]:
+        with pytest.raises(g.GrinqhError):
+            g.grinqh_topk_counts(K, p)
+
+
+# Device entry points, given arguments that fail host validation ---------------
+FAKE = ctypes.c_void_p(0x1000)   # never dereferenced: every call below fails validation
+
+
+def _call_pack(g, d, kind, src, sc, pc, ps):
+    return g.lib.grinqh_pack(ctypes.byref(d), kind, src, sc, pc, ps, None)
+
+
+def test_pack_validation(g):
+    d = g.make_desc(256, 512, (0, 2, 4, 8))
+    assert _call_pack(g, d, 7, FAKE, None, FAKE, FAKE) == -1
+    assert _call_pack(g, d, 0, None, None, FAKE, FAKE) == -1
+    assert _call_pack(g, d, 0, FAKE, FAKE, FAKE, FAKE) == -1       # scales given for fp16
+    assert _call_pack(g, d, 1, FAKE, None, FAKE, FAKE) == -1       # scales missing for codes
+    bad = g.make_desc(250, 512, (0, 2, 4, 8))
+    assert _call_pack(g, bad, 0, FAKE, None, FAKE, FAKE) == -1
+
+
+def _th(vals):
+    return (ctypes.c_float * len(vals))(*vals)
+
+
+def _cn(vals):
+    return (ctypes.c_int32 * len(vals))(*vals)
+
+
+def test_assign_validation(g):
+    d = g.make_desc(256, 512, (0, 2, 4, 8))
+    A = g.lib.grinqh_assign
+    assert A(ctypes.byref(d), 0, FAKE, 0, _th([1, 2, 3]), None, FAKE, None, 0, None) == -1
+    assert A(ctypes.byref(d), 0, None, 1, _th([1, 2, 3]), None, FAKE, None, 0, None) == -1
+    assert A(ctypes.byref(d), 0, FAKE, 1, None, None, FAKE, None, 0, None) == -1
+    assert A(ctypes.byref(d), 0, FAKE, 1, _th([1, 3, 2]), None, FAKE, None, 0, None) == -1
+    assert A(ctypes.byref(d), 0, FAKE, 1, _th([1, float("nan"), 2]), None, FAKE, None, 0, None) == -1
+    assert A(ctypes.byref(d), 0, FAKE, 1, _th([1, 2, 3]), _cn([1, 1, 1, 253]), FAKE, None, 0, None) == -1
+    assert A(ctypes.byref(d), 1, FAKE, 1, None, None, FAKE, None, 0, None) == -1
+    assert A(ctypes.byref(d), 1, FAKE, 1, None, _cn([1, 1, 1, 1]), FAKE, None, 0, None) == -1
+    assert A(ctypes.byref(d), 1, FAKE, 1, None, _cn([-1, 1, 1, 255]), FAKE, None, 0, None) == -1
+    assert A(ctypes.byref(d), 1, FAKE, 1, _th([1, 2, 3]), _cn([64, 64, 64, 64]), FAKE, None, 0, None) == -1
+    assert A(ctypes.byref(d), 5, FAKE, 1, None, None, FAKE, None, 0, None) == -1
+    big = g.make_desc(128 * 1024, 512, (0, 8))
+    assert A(ctypes.byref(big), 1, FAKE, 1, None, _cn([0, 128 * 1024]), FAKE, None, 0, None) == -2
+
+
+def test_vmm_validation(g):
+    d = g.make_desc(256, 512, (0, 2, 4, 8))
+    V = g.lib.grinqh_vmm
+    assert V(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, 0, FAKE, 0, None, 0, None) == -2
+    assert V(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, 5, FAKE, 0, None, 0, None) == -2
+    assert V(ctypes.byref(d), FAKE, FAKE, FAKE, None, 1, FAKE, 0, None, 0, None) == -1
+    assert V(ctypes.byref(d), None, FAKE, FAKE, FAKE, 1, FAKE, 0, None, 0, None) == -1
+    assert V(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, 1, FAKE, 4, None, 0, None) == -1
+    VT = g.lib.grinqh_vmm_threshold
+    assert VT(ctypes.byref(d), FAKE, FAKE, FAKE, 1, None, None, FAKE, 0, None, 0, None) == -1
+    assert VT(ctypes.byref(d), FAKE, FAKE, FAKE, 1, _th([2, 1, 3]), None, FAKE, 0, None, 0, None) == -1
+    assert VT(ctypes.byref(d), FAKE, FAKE, FAKE, 9, _th([1, 2, 3]), None, FAKE, 0, None, 0, None) == -2
+    assert g.grinqh_last_error()
+
+
+def test_binding_rejects_host_tensors(g):
+    import torch
+    d = g.make_desc(256, 512, (0, 2, 4, 8))
+    with pytest.raises(ValueError):
+        g.grinqh_pack(d, W=torch.zeros(512, 256, dtype=torch.float16))

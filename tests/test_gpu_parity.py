@@ -1,0 +1,281 @@
+"""GPU parity of libgrinqh against the CPU oracle (run on an MI355X).
+
+Bars: packed codes, scales and level maps bit-exact; y within max-normwise
+relative error 1e-3 of the float64 oracle (max_n |y - y_ref| / max_n |y_ref|).
+All calls go through the C ABI via the thin binding.
+"""
+import numpy as np
+import pytest
+
+from oracle import grinqh_oracle as orc
+from synth import inputs
+
+pytestmark = pytest.mark.gpu
+TOL = 1e-3
+
+
+@pytest.fixture(scope="module")
+def g():
+    from paper_2606_23419_amd import grinqh
+    return grinqh
+
+
+@pytest.fixture(scope="module")
+def torch():
+    import torch as t
+    assert t.cuda.is_available()
+    return t
+
+
+def _dev(torch, a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def _host(t):
+    return t.detach().cpu().numpy()
+
+
+def normwise(y, ref):
+    ref = np.asarray(ref, dtype=np.float64)
+    den = np.max(np.abs(ref))
+    num = np.max(np.abs(np.asarray(y, dtype=np.float64) - ref))
+    return num / den if den > 0 else num
+
+
+class Layer:
+    """One packed layer: GPU buffers and the oracle's codes/scales."""
+
+    def __init__(self, g, torch, K, N, levels, cfg=50, layer=0, tile_n=0, codes_src=False):
+        self.desc = g.grinqh_resolve_desc(g.make_desc(K, N, levels, tile_n=tile_n))
+        self.levels = tuple(levels)
+        self.K, self.N = K, N
+        if codes_src:
+            self.codes = inputs.random_codes(N, K, cfg, layer)
+            sc_nk = inputs.random_scales(N, K, 128, cfg, layer)
+            self.scales = np.ascontiguousarray(sc_nk.T)
+            self.pc, self.ps = g.grinqh_pack(self.desc, codes=_dev(torch, self.codes),
+                                             scales=_dev(torch, sc_nk))
+        else:
+            W = inputs.weights(N, K, cfg, layer)
+            self.codes, self.scales = orc.rtn_quantize(W)
+            self.pc, self.ps = g.grinqh_pack(self.desc, W=_dev(torch, W))
+        torch.cuda.synchronize()
+
+    def check_packed(self):
+        u, T = self.desc.plane_bits, self.desc.tile_n
+        want = orc.pack_codes_fast(self.codes, u, T)
+        got = _host(self.pc)
+        assert np.array_equal(got, want), f"packed codes differ at {np.nonzero(got != want)[0][:8]}"
+        assert np.array_equal(_host(self.ps).view(np.uint16), self.scales.view(np.uint16))
+
+
+# ------------------------------------------------------------------ pack ----
+@pytest.mark.parametrize("K,N,levels,tile_n", [
+    (128, 512, (0, 2, 4, 8), 0), (640, 1024, (0, 2, 4, 6, 8), 256), (256, 2048, (0, 2, 3, 4, 8), 0),
+    (384, 2048, (0, 2, 4, 8), 2048), (256, 1024, (0, 2, 3, 4, 8), 1024)])
+def test_pack_rtn_bit_exact(g, torch, K, N, levels, tile_n):
+    Layer(g, torch, K, N, levels, tile_n=tile_n).check_packed()
+
+
+def test_pack_codes_source_bit_exact(g, torch):
+    Layer(g, torch, 512, 1024, (0, 2, 4, 6, 8), codes_src=True).check_packed()
+    Layer(g, torch, 256, 512, (0, 2, 3, 4, 8), codes_src=True).check_packed()
+
+
+def test_pack_rtn_edge_groups(g, torch):
+    # zero groups, a subnormal-only group (scale underflows to 0), ties
+    K, N = 256, 512
+    W = inputs.weights(N, K, 51).copy()
+    W[0, :128] = 0.0
+    W[1, :128] = np.float16(2.0 ** -23)
+    W[2, :] = np.float16(127.0)
+    W[2, 1:5] = np.array([2.5, 3.5, -2.5, -0.0], dtype=np.float16)
+    desc = g.grinqh_resolve_desc(g.make_desc(K, N, (0, 2, 4, 8)))
+    pc, ps = g.grinqh_pack(desc, W=_dev(torch, W))
+    q, s = orc.rtn_quantize(W)
+    assert np.array_equal(_host(pc), orc.pack_codes_fast(q, 2, desc.tile_n))
+    assert np.array_equal(_host(ps).view(np.uint16), s.view(np.uint16))
+
+
+# ---------------------------------------------------------------- assign ----
+@pytest.mark.parametrize("K", [128, 640, 4096, 14336])
+def test_assign_threshold_bit_exact(g, torch, K):
+    desc = g.make_desc(K, 512, (0, 2, 4, 6, 8))
+    x = inputs.activations_t3(K, 3, 52)
+    th = np.array([0.3, 0.7, 1.5, 4.0], dtype=np.float32)
+    x[0, :4] = np.array([0.3, -0.7, 1.5, 4.0], dtype=np.float16).astype(np.float16)
+    lm = g.grinqh_assign(desc, _dev(torch, x), g.GRINQH_ASSIGN_THRESHOLD, thresholds=th)
+    assert np.array_equal(_host(lm), orc.assign_threshold(x, th))
+
+
+@pytest.mark.parametrize("K", [128, 640, 1024, 4096, 14336])
+@pytest.mark.parametrize("levels", [(0, 2, 4, 8), (0, 2, 4, 6, 8), (0, 2, 3, 4, 8)])
+def test_assign_topk_bit_exact(g, torch, K, levels):
+    desc = g.make_desc(K, 512, levels)
+    x = inputs.activations_t3(K, 4, 53) if K != 14336 else inputs.activations_swiglu(K, 4, 53)
+    for p in inputs.BUDGETS[tuple(levels)].values():
+        counts = g.grinqh_topk_counts(K, p)
+        lm = g.grinqh_assign(desc, _dev(torch, x), g.GRINQH_ASSIGN_TOPK, counts=counts)
+        assert np.array_equal(_host(lm), orc.assign_topk(x, counts))
+
+
+@pytest.mark.parametrize("case", ["ties", "all_equal", "zeros", "signed_zero", "extreme_counts"])
+def test_assign_topk_adversarial(g, torch, case):
+    K = 1024
+    rng = np.random.default_rng(54)
+    desc = g.make_desc(K, 512, (0, 2, 4, 8))
+    if case == "ties":
+        x = rng.choice(np.array([0.5, -0.5, 1.0, 2.0, -2.0, 0.0], np.float16), size=(3, K))
+    elif case == "all_equal":
+        x = np.full((2, K), -1.25, dtype=np.float16)
+    elif case == "zeros":
+        x = np.zeros((2, K), dtype=np.float16)
+    elif case == "signed_zero":
+        x = np.where(rng.random((2, K)) < 0.5, np.float16(0.0), np.float16(-0.0)).astype(np.float16)
+        x[:, ::7] = np.float16(3.0)
+    else:
+        x = inputs.activations_t3(K, 2, 55)
+    x = x.astype(np.float16)
+    plist = [(2000, 2000, 3000, 3000), (0, 0, 0, 10000), (10000, 0, 0, 0), (3333, 3333, 3334, 0)]
+    for p in plist:
+        counts = g.grinqh_topk_counts(K, p)
+        lm = g.grinqh_assign(desc, _dev(torch, x), g.GRINQH_ASSIGN_TOPK, counts=counts)
+        assert np.array_equal(_host(lm), orc.assign_topk(x, counts)), (case, p)
+    # counts of a single channel at each level
+    counts = [K - 3, 1, 1, 1]
+    lm = g.grinqh_assign(desc, _dev(torch, x), g.GRINQH_ASSIGN_TOPK, counts=counts)
+    assert np.array_equal(_host(lm), orc.assign_topk(x, counts))
+
+
+# ------------------------------------------------------------------- vmm ----
+def _vmm_case(g, torch, L, x, lm):
+    y = g.grinqh_vmm(L.desc, L.pc, L.ps, _dev(torch, x), _dev(torch, lm))
+    torch.cuda.synchronize()
+    ref = orc.vmm_batch(L.codes, L.scales, x, lm, L.levels)
+    return _host(y), ref
+
+
+@pytest.mark.parametrize("K,N,levels,tile_n", [
+    (128, 512, (0, 2, 4, 8), 0), (640, 1024, (0, 2, 4, 6, 8), 256), (1024, 1024, (0, 2, 4, 8), 0),
+    (384, 2048, (0, 2, 3, 4, 8), 0), (896, 2048, (0, 2, 4, 6, 8), 1024), (256, 2048, (0, 2, 4, 8), 2048)])
+@pytest.mark.parametrize("B", [1, 2, 4])
+def test_vmm_topk_parity(g, torch, K, N, levels, tile_n, B):
+    L = Layer(g, torch, K, N, levels, tile_n=tile_n)
+    x = inputs.activations_t3(K, B, 56, 1)
+    for p in inputs.BUDGETS[tuple(levels)].values():
+        counts = g.grinqh_topk_counts(K, p)
+        lm = _host(g.grinqh_assign(L.desc, _dev(torch, x), g.GRINQH_ASSIGN_TOPK, counts=counts))
+        y, ref = _vmm_case(g, torch, L, x, lm)
+        assert normwise(y, ref) <= TOL, (p, normwise(y, ref))
+
+
+@pytest.mark.parametrize("levels", [(0, 2, 4, 8), (0, 2, 4, 6, 8), (0, 2, 3, 4, 8)])
+def test_vmm_random_level_maps(g, torch, levels):
+    K, N = 1152, 1024
+    L = Layer(g, torch, K, N, levels, cfg=57)
+    rng = np.random.default_rng(57)
+    for B in (1, 3):
+        x = inputs.activations_t3(K, B, 57, 2)
+        lm = rng.integers(0, len(levels), size=(B, K)).astype(np.uint8)
+        y, ref = _vmm_case(g, torch, L, x, lm)
+        assert normwise(y, ref) <= TOL
+
+
+def test_vmm_all_skipped_is_exactly_zero(g, torch):
+    L = Layer(g, torch, 512, 1024, (0, 2, 4, 8), cfg=58)
+    x = inputs.activations_t3(512, 2, 58)
+    y, _ = _vmm_case(g, torch, L, x, np.zeros((2, 512), np.uint8))
+    assert np.all(y == 0.0)
+
+
+def test_vmm_all_top_is_dequant_matvec(g, torch):
+    L = Layer(g, torch, 512, 1024, (0, 2, 4, 8), cfg=59)
+    x = inputs.activations_t3(512, 1, 59)
+    y, _ = _vmm_case(g, torch, L, x, np.full((1, 512), 3, np.uint8))
+    s_full = np.repeat(L.scales.astype(np.float64).T, 128, axis=1)
+    ref = (s_full * (L.codes.astype(np.float64) - 128)) @ x[0].astype(np.float64)
+    assert normwise(y[0], ref) <= TOL
+
+
+def test_vmm_single_level_and_mixed_tokens(g, torch):
+    levels = (0, 2, 4, 6, 8)
+    L = Layer(g, torch, 768, 1024, levels, cfg=60)
+    x = inputs.activations_t3(768, 4, 60)
+    lm = np.stack([np.full(768, j, np.uint8) for j in (1, 2, 3, 4)])
+    y, ref = _vmm_case(g, torch, L, x, lm)
+    for t in range(4):
+        assert normwise(y[t], ref[t]) <= TOL
+
+
+def test_vmm_batch_equals_single_tokens(g, torch):
+    levels = (0, 2, 4, 6, 8)
+    L = Layer(g, torch, 1024, 1024, levels, cfg=61)
+    x = inputs.activations_t3(1024, 4, 61)
+    rng = np.random.default_rng(61)
+    lm = rng.integers(0, 5, size=(4, 1024)).astype(np.uint8)
+    yb, ref = _vmm_case(g, torch, L, x, lm)
+    for t in range(4):
+        y1, _ = _vmm_case(g, torch, L, x[t:t + 1], lm[t:t + 1])
+        assert normwise(y1[0], ref[t]) <= TOL
+        assert normwise(yb[t], ref[t]) <= TOL
+
+
+def test_vmm_accumulate_flag_and_clamped_levels(g, torch):
+    L = Layer(g, torch, 512, 512, (0, 2, 4, 8), cfg=62)
+    x = inputs.activations_t3(512, 1, 62)
+    lm = np.random.default_rng(62).integers(0, 4, size=(1, 512)).astype(np.uint8)
+    y0 = torch.full((1, 512), 1.5, dtype=torch.float32, device="cuda")
+    g.grinqh_vmm(L.desc, L.pc, L.ps, _dev(torch, x), _dev(torch, lm), y=y0, accumulate=True)
+    ref = orc.vmm_batch(L.codes, L.scales, x, lm, L.levels) + 1.5
+    assert normwise(_host(y0), ref) <= TOL
+    # a level value above the top level is read as the top level
+    lm_hi = lm.copy()
+    lm_hi[lm_hi == 3] = 200
+    y, _ = _vmm_case(g, torch, L, x, lm_hi)
+    assert normwise(y, orc.vmm_batch(L.codes, L.scales, x, lm, L.levels)) <= TOL
+
+
+@pytest.mark.parametrize("levels", [(0, 2, 4, 8), (0, 2, 3, 4, 8)])
+def test_vmm_threshold_fused(g, torch, levels):
+    K, N = 1024, 1024
+    L = Layer(g, torch, K, N, levels, cfg=63)
+    x = inputs.activations_t3(K, 3, 63)
+    th = np.sort(np.abs(x[0].astype(np.float32)))[[300, 500, 800, 1000][:len(levels) - 1]]
+    lm_out = torch.zeros((3, K), dtype=torch.uint8, device="cuda")
+    y = g.grinqh_vmm_threshold(L.desc, L.pc, L.ps, _dev(torch, x), th, level_map_out=lm_out)
+    torch.cuda.synchronize()
+    lm = orc.assign_threshold(x, th)
+    assert np.array_equal(_host(lm_out), lm)
+    ref = orc.vmm_batch(L.codes, L.scales, x, lm, levels)
+    assert normwise(_host(y), ref) <= TOL
+
+
+# ------------------------------------------ full-size workload shapes ----
+FULL = [
+    ("cfg1 1024x1024", 1024, 1024, inputs.LEVELS_A, "t3"),
+    ("cfg2 q 4096x4096", 4096, 4096, inputs.LEVELS_B, "t3"),
+    ("cfg2 k 4096->1024", 4096, 1024, inputs.LEVELS_B, "t3"),
+    ("cfg3 up 4096->14336", 4096, 14336, inputs.LEVELS_B, "t3"),
+    ("cfg3 down 14336->4096", 14336, 4096, inputs.LEVELS_B, "swiglu"),
+    ("cfg4 qkv 4096->6144", 4096, 6144, inputs.LEVELS_C, "t3"),
+    ("cfg4 down 12288->4096", 12288, 4096, inputs.LEVELS_C, "swiglu"),
+]
+
+
+@pytest.mark.parametrize("name,K,N,levels,xkind", FULL, ids=[f[0] for f in FULL])
+def test_full_size_pack_and_sampled_vmm(g, torch, name, K, N, levels, xkind):
+    L = Layer(g, torch, K, N, levels, cfg=70, layer=K + N)
+    L.check_packed()
+    gen = inputs.activations_swiglu if xkind == "swiglu" else inputs.activations_t3
+    x = gen(K, 2, 70, K + N)
+    rows = np.sort(np.random.default_rng(K + N).choice(N, size=96, replace=False))
+    for p in inputs.BUDGETS[tuple(levels)].values():
+        counts = g.grinqh_topk_counts(K, p)
+        lm = g.grinqh_assign(L.desc, _dev(torch, x), g.GRINQH_ASSIGN_TOPK, counts=counts)
+        lm_h = _host(lm)
+        assert np.array_equal(lm_h, orc.assign_topk(x, counts))
+        y = _host(g.grinqh_vmm(L.desc, L.pc, L.ps, _dev(torch, x), lm))
+        ref = orc.vmm_batch(L.codes[rows], L.scales[:, rows], x, lm_h, levels)
+        # sampled outputs against the oracle, and the whole vector's scale
+        assert normwise(y[:, rows], ref) <= TOL, (name, p)
+        assert np.all(np.isfinite(y))
