@@ -178,8 +178,10 @@ def main():
         graph.replay()
         torch.cuda.synchronize()
         for n, b in ybufs.items():
-            if not torch.allclose(b, eager[n], rtol=1e-5, atol=1e-4):
-                raise RuntimeError(f"graph replay of {n} differs from the eager step")
+            # partial sums meet in atomics, so replays agree to rounding, not bits
+            err = float((b - eager[n]).abs().max() / eager[n].abs().max())
+            if not err <= 1e-5:
+                raise RuntimeError(f"graph replay of {n} differs from the eager step ({err:.2e})")
     for m, h in zip(lm, lm_host):
         if not np.array_equal(m.cpu().numpy(), h):
             raise RuntimeError("graph replay changed a level map")

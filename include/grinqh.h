@@ -122,7 +122,7 @@ GRINQH_API int grinqh_workspace_bytes(const grinqh_layer_desc* desc, int32_t B, 
  *   mode GRINQH_ASSIGN_TOPK: counts = host int32 c_0..c_n summing to K (e.g.
  *     from grinqh_topk_counts).  Channels are ordered by |x| descending, ties
  *     by lower index; the first c_n get level n, the next c_{n-1} level n-1,
- *     and so on.  thresholds = NULL.  Requires K <= 65536.
+ *     and so on.  thresholds = NULL.  Requires K <= 16384.
  *   level_map: uint8 [B][K] (device), the level index per channel. */
 GRINQH_API int grinqh_assign(const grinqh_layer_desc* desc, int mode, const void* x, int32_t B,
                   const float* thresholds, const int32_t* counts, uint8_t* level_map,

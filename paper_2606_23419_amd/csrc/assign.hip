@@ -21,112 +21,183 @@ __global__ __launch_bounds__(256) void k_assign_threshold(const uint16_t* __rest
   lm[i] = (uint8_t)l;
 }
 
-// Top-k: one workgroup of 1024 threads per token.  For every level j the cut
-// is the C_j-th largest key (C_j = channels at level >= j), found by a
-// two-digit radix select (8 high bits, then 7 low bits) with LDS histograms
-// for all levels at once.  Channels strictly above the cut key are in; of
-// the channels equal to it, the lowest indices are in, counted in index order
-// with a ballot + mbcnt prefix inside each wave and a scan over waves.
+// Top-k: one workgroup of 1024 threads per token, every key in registers
+// (K <= 16384).  For every level j the cut is the C_j-th largest key (C_j =
+// channels at level >= j).  A two-digit radix select finds all cuts at once:
+// per-wave LDS histograms of the high 8 bits, a parallel suffix scan to find
+// the bin holding each cut, then 128-bin histograms of the low 7 bits inside
+// those bins.  Channels strictly above the cut key are in.  Of the channels
+// equal to it, the first ones in index order are in: per-(chunk, wave) ballots
+// of key == cut are stored, and one wave per level walks them in index order
+// to find the channel index where the count reaches the number still needed.
 constexpr int kTopkThreads = 1024;
 constexpr int kTopkWaves = kTopkThreads / 64;
+constexpr int kTopkPer = 16;                     // keys per thread
+constexpr int kTopkMaxK = kTopkThreads * kTopkPer;
+constexpr int kCuts = kMaxLevels - 1;
+
+__device__ __forceinline__ uint32_t incl_scan64(uint32_t v, int lane) {
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const uint32_t o = __shfl_up(v, off);
+    if (lane >= off) v += o;
+  }
+  return v;
+}
+
+// Position (0..63) of the r-th set bit (r >= 1) of m.
+__device__ __forceinline__ int nth_set_bit(uint64_t m, int r) {
+  int pos = 0;
+#pragma unroll
+  for (int w = 32; w > 0; w >>= 1) {
+    const uint64_t low = m & ((w == 64 ? ~0ull : (1ull << w) - 1ull));
+    const int c = __popcll(low);
+    if (r > c) {
+      r -= c;
+      m >>= w;
+      pos += w;
+    } else {
+      m = low;
+    }
+  }
+  return pos;
+}
 
 __global__ __launch_bounds__(kTopkThreads) void k_assign_topk(const uint16_t* __restrict__ x,
                                                               uint8_t* __restrict__ lm, int K,
                                                               TopkCuts cuts) {
-  __shared__ uint32_t hist1[256];
-  __shared__ uint32_t hist2[kMaxLevels - 1][128];
-  __shared__ int cut_bin[kMaxLevels - 1], need_bin[kMaxLevels - 1];
-  __shared__ uint32_t cut_key[kMaxLevels - 1];
-  __shared__ int need_eq[kMaxLevels - 1];
-  __shared__ uint32_t wave_eq[kTopkWaves][kMaxLevels - 1];
-  __shared__ uint32_t running[kMaxLevels - 1];
+  __shared__ uint32_t s_h1[kTopkWaves][256];
+  __shared__ uint32_t s_h2[kCuts][128];
+  __shared__ uint32_t s_wsum[kTopkWaves];
+  __shared__ int s_cut_bin[kCuts], s_need[kCuts], s_need_eq[kCuts], s_idx_lim[kCuts];
+  __shared__ uint32_t s_cut_key[kCuts];
+  __shared__ uint64_t s_bal[kTopkPer][kTopkWaves][kCuts];
 
-  const int tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int n = cuts.n;
+  const int M = (K + kTopkThreads - 1) / kTopkThreads;
   const uint16_t* xt = x + (size_t)blockIdx.x * K;
   uint8_t* out = lm + (size_t)blockIdx.x * K;
 
-  for (int i = tid; i < 256; i += kTopkThreads) hist1[i] = 0;
-  for (int i = tid; i < (kMaxLevels - 1) * 128; i += kTopkThreads) (&hist2[0][0])[i] = 0;
-  if (tid < kMaxLevels - 1) running[tid] = 0;
-  __syncthreads();
-
-  for (int k = tid; k < K; k += kTopkThreads) atomicAdd(&hist1[mag_key(xt[k]) >> 7], 1u);
-  __syncthreads();
-
-  if (tid < n) {
-    const int C = cuts.cum[tid];
-    int bin = 256, need = 0;
-    if (C > 0) {
-      int acc = 0;
-      for (int b = 255; b >= 0; --b) {
-        const int h = (int)hist1[b];
-        if (acc + h >= C) { bin = b; need = C - acc; break; }
-        acc += h;
-      }
-    }
-    cut_bin[tid] = bin;
-    need_bin[tid] = need;
+  uint32_t key[kTopkPer];
+#pragma unroll
+  for (int m = 0; m < kTopkPer; ++m) {
+    const int k = m * kTopkThreads + tid;
+    key[m] = (m < M && k < K) ? mag_key(xt[k]) : 0xFFFFu;   // 0xFFFF: no channel
+  }
+  for (int i = tid; i < kTopkWaves * 256; i += kTopkThreads) (&s_h1[0][0])[i] = 0u;
+  for (int i = tid; i < kCuts * 128; i += kTopkThreads) (&s_h2[0][0])[i] = 0u;
+  if (tid < kCuts) {
+    s_cut_bin[tid] = 256;
+    s_need[tid] = 0;
+    s_cut_key[tid] = 0x8000u;   // above every key: nobody is in
+    s_need_eq[tid] = 0;
+    s_idx_lim[tid] = 0;
   }
   __syncthreads();
 
-  for (int k = tid; k < K; k += kTopkThreads) {
-    const uint32_t key = mag_key(xt[k]);
-    const int bin = (int)(key >> 7);
+  // high-digit histograms, one per wave
+#pragma unroll
+  for (int m = 0; m < kTopkPer; ++m)
+    if (key[m] != 0xFFFFu) atomicAdd(&s_h1[wave][key[m] >> 7], 1u);
+  __syncthreads();
+
+  // suffix counts over bins: thread i < 256 takes bin 255 - i
+  uint32_t tot = 0, incl = 0;
+  if (tid < 256) {
+    const int b = 255 - tid;
+    for (int w = 0; w < kTopkWaves; ++w) tot += s_h1[w][b];
+    incl = incl_scan64(tot, lane);
+    if (lane == 63) s_wsum[wave] = incl;
+  }
+  __syncthreads();
+  if (tid < 256) {
+    for (int w = 0; w < wave; ++w) incl += s_wsum[w];
+    const uint32_t above = incl - tot;   // keys in higher bins
+    for (int j = 0; j < n; ++j) {
+      const uint32_t C = (uint32_t)cuts.cum[j];
+      if (C > above && C <= incl) {
+        s_cut_bin[j] = 255 - tid;
+        s_need[j] = (int)(C - above);
+      }
+    }
+  }
+  __syncthreads();
+
+  // low-digit histograms inside each cut bin
+#pragma unroll
+  for (int m = 0; m < kTopkPer; ++m) {
+    if (key[m] == 0xFFFFu) continue;
+    const int hi = (int)(key[m] >> 7);
     for (int j = 0; j < n; ++j)
-      if (bin == cut_bin[j]) atomicAdd(&hist2[j][key & 127u], 1u);
+      if (hi == s_cut_bin[j]) atomicAdd(&s_h2[j][key[m] & 127u], 1u);
   }
   __syncthreads();
 
-  if (tid < n) {
-    uint32_t ck = 0x8000u;   // above every key: nobody is in
-    int need = 0;
-    if (cut_bin[tid] < 256) {
-      int acc = 0;
-      for (int s = 127; s >= 0; --s) {
-        const int h = (int)hist2[tid][s];
-        if (acc + h >= need_bin[tid]) { ck = ((uint32_t)cut_bin[tid] << 7) | (uint32_t)s; need = need_bin[tid] - acc; break; }
-        acc += h;
+  // per level j (threads 128 j .. 128 j + 127), suffix over sub-bins
+  {
+    const int j = tid >> 7, i = tid & 127, sb = 127 - i;
+    const uint32_t h = j < n ? s_h2[j][sb] : 0u;
+    uint32_t inc2 = incl_scan64(h, lane);
+    if (lane == 63) s_wsum[wave] = inc2;
+    __syncthreads();
+    if (wave & 1) inc2 += s_wsum[wave - 1];
+    if (j < n && s_cut_bin[j] < 256) {
+      const uint32_t need = (uint32_t)s_need[j];
+      const uint32_t above = inc2 - h;
+      if (need > above && need <= inc2) {
+        s_cut_key[j] = ((uint32_t)s_cut_bin[j] << 7) | (uint32_t)sb;
+        s_need_eq[j] = (int)(need - above);
       }
     }
-    cut_key[tid] = ck;
-    need_eq[tid] = need;
   }
   __syncthreads();
 
-  for (int base = 0; base < K; base += kTopkThreads) {
-    const int k = base + tid;
-    const bool valid = k < K;
-    const uint32_t key = valid ? mag_key(xt[k]) : 0u;
-    uint32_t pre[kMaxLevels - 1];
-    bool eq[kMaxLevels - 1];
+  // ballots of key == cut key, per (chunk, wave, level)
 #pragma unroll
-    for (int j = 0; j < kMaxLevels - 1; ++j) {
-      eq[j] = valid && j < n && key == cut_key[j];
-      const uint64_t bal = __ballot(eq[j]);
-      pre[j] = __builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32),
-                                         __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u));
-      if (lane == 0) wave_eq[wave][j] = (uint32_t)__popcll(bal);
+  for (int m = 0; m < kTopkPer; ++m) {
+    if (m >= M) break;
+    for (int j = 0; j < n; ++j) {
+      const uint64_t bal = __ballot(key[m] == s_cut_key[j]);
+      if (lane == 0) s_bal[m][wave][j] = bal;
     }
-    __syncthreads();
+  }
+  __syncthreads();
+
+  // wave j finds the index of the need_eq-th channel equal to cut key j
+  if (wave < n) {
+    const int j = wave;
+    const int need = s_need_eq[j];
+    const int E = M * kTopkWaves;
+    int carry = 0;
+    for (int base = 0; base < E && need > 0; base += 64) {
+      const int e = base + lane;
+      const uint64_t bal = e < E ? s_bal[e / kTopkWaves][e % kTopkWaves][j] : 0ull;
+      const uint32_t c = (uint32_t)__popcll(bal);
+      const uint32_t inc = incl_scan64(c, lane) + (uint32_t)carry;
+      const uint32_t before = inc - c;
+      if ((uint32_t)need > before && (uint32_t)need <= inc) {
+        const int bit = nth_set_bit(bal, need - (int)before);
+        // entry e covers channels (e / 16) * 1024 + (e % 16) * 64 + bit
+        s_idx_lim[j] = (e / kTopkWaves) * kTopkThreads + (e % kTopkWaves) * 64 + bit + 1;
+      }
+      carry = (int)__shfl(inc, 63);
+      if (carry >= need) break;
+    }
+  }
+  __syncthreads();
+
+#pragma unroll
+  for (int m = 0; m < kTopkPer; ++m) {
+    if (m >= M) break;
+    const int k = m * kTopkThreads + tid;
+    if (k >= K) continue;
     int lvl = 0;
-#pragma unroll
-    for (int j = 0; j < kMaxLevels - 1; ++j) {
-      if (j >= n) break;
-      uint32_t before = running[j];
-      for (int w = 0; w < wave; ++w) before += wave_eq[w][j];
-      const bool in = valid && (key > cut_key[j] || (eq[j] && (int)(before + pre[j]) < need_eq[j]));
-      lvl += in ? 1 : 0;
+    for (int j = 0; j < n; ++j) {
+      const uint32_t ck = s_cut_key[j];
+      lvl += (key[m] > ck || (key[m] == ck && k < s_idx_lim[j])) ? 1 : 0;
     }
-    __syncthreads();
-    if (tid < n) {
-      uint32_t tot = 0;
-      for (int w = 0; w < kTopkWaves; ++w) tot += wave_eq[w][tid];
-      running[tid] += tot;
-    }
-    if (valid) out[k] = (uint8_t)lvl;
-    __syncthreads();
+    out[k] = (uint8_t)lvl;
   }
 }
 

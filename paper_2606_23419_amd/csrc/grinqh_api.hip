@@ -68,9 +68,11 @@ static int resolve(const grinqh_layer_desc* d, Layer* L, grinqh_layer_desc* out)
   if (L) {
     L->K = d->K; L->N = d->N; L->n_levels = nl; L->u = u; L->P = 8 / u; L->T = T;
     L->tiles = d->N / T; L->groups = d->K / kGroup;
+    L->planes_packed = 0;
     for (int i = 0; i < kMaxLevels; ++i) {
       L->bits[i] = i < nl ? d->level_bits[i] : 0;
       L->planes[i] = i < nl ? d->level_bits[i] / u : 0;
+      L->planes_packed |= (uint64_t)L->planes[i] << (4 * i);
     }
   }
   if (out) {
@@ -182,7 +184,7 @@ int grinqh_assign(const grinqh_layer_desc* desc, int mode, const void* x, int32_
   if (mode == GRINQH_ASSIGN_TOPK) {
     if (thresholds) return fail(GRINQH_EINVAL, "thresholds must be NULL in top-k mode");
     if (!counts) return fail(GRINQH_EINVAL, "counts is NULL");
-    if (L.K > 65536) return fail(GRINQH_EUNSUPPORTED, "top-k assignment needs K <= 65536 (K=%d)", L.K);
+    if (L.K > 16384) return fail(GRINQH_EUNSUPPORTED, "top-k assignment needs K <= 16384 (K=%d)", L.K);
     long long total = 0;
     for (int j = 0; j < L.n_levels; ++j) {
       if (counts[j] < 0) return fail(GRINQH_EINVAL, "counts[%d]=%d is negative", j, counts[j]);
@@ -207,6 +209,9 @@ static int vmm_common_checks(const Layer& L, const void* codes, const void* scal
   if (!codes || !scales || !x || !y) return fail(GRINQH_EINVAL, "codes, scales, x and y must not be NULL");
   if (B < 1 || B > kMaxB) return fail(GRINQH_EUNSUPPORTED, "B=%d outside 1..%d", B, kMaxB);
   if (flags & ~GRINQH_VMM_ACCUMULATE) return fail(GRINQH_EINVAL, "unknown flags 0x%x", flags);
+  if (((uintptr_t)codes | (uintptr_t)scales) & 15u)
+    return fail(GRINQH_EINVAL, "packed codes and scales must be 16-byte aligned");
+  if (((uintptr_t)x | (uintptr_t)y) & 3u) return fail(GRINQH_EINVAL, "x and y must be 4-byte aligned");
   (void)L;
   return GRINQH_OK;
 }
@@ -222,6 +227,7 @@ int grinqh_vmm(const grinqh_layer_desc* desc, const void* packed_codes, const vo
   st = vmm_common_checks(L, packed_codes, packed_scales, x, B, y, flags);
   if (st) return st;
   if (!level_map) return fail(GRINQH_EINVAL, "level_map is NULL");
+  if ((uintptr_t)level_map & 1u) return fail(GRINQH_EINVAL, "level_map must be 2-byte aligned");
   return launch_vmm(L, packed_codes, packed_scales, x, level_map, nullptr, nullptr, B, y,
                     flags & GRINQH_VMM_ACCUMULATE, (hipStream_t)stream);
 }
@@ -240,6 +246,7 @@ int grinqh_vmm_threshold(const grinqh_layer_desc* desc, const void* packed_codes
   Thresholds th;
   st = check_thresholds(L, thresholds, &th);
   if (st) return st;
+  if ((uintptr_t)level_map_out & 1u) return fail(GRINQH_EINVAL, "level_map_out must be 2-byte aligned");
   return launch_vmm(L, packed_codes, packed_scales, x, nullptr, &th, level_map_out, B, y,
                     flags & GRINQH_VMM_ACCUMULATE, (hipStream_t)stream);
 }

@@ -23,7 +23,15 @@ struct Layer {
   int groups;       // K / 128
   int bits[kMaxLevels];    // b_l
   int planes[kMaxLevels];  // b_l / u: planes read at level l
+  // planes[l] in bits 4l..4l+3.  Kernels index levels per lane; a by-value
+  // array indexed that way is read from kernel-argument memory one lane at a
+  // time, while this word is one scalar register pair.
+  uint64_t planes_packed;
 };
+
+__host__ __device__ __forceinline__ int level_planes(uint64_t packed, int level) {
+  return (int)((packed >> (4 * level)) & 0xFu);
+}
 
 struct Thresholds {
   float theta[kMaxLevels - 1];   // theta_1 .. theta_n
@@ -54,6 +62,10 @@ int launch_assign_threshold(const Layer& L, const void* x, int B, const Threshol
                             uint8_t* level_map, hipStream_t s);
 int launch_assign_topk(const Layer& L, const void* x, int B, const TopkCuts& cuts,
                        uint8_t* level_map, hipStream_t s);
+bool vmm_dot2_supported(const Layer& L);
+int launch_vmm_dot2(const Layer& L, const void* codes, const void* scales, const void* x,
+                    const uint8_t* level_map, const Thresholds* th, uint8_t* level_map_out,
+                    int B, float* y, hipStream_t s);
 int launch_vmm(const Layer& L, const void* codes, const void* scales, const void* x,
                const uint8_t* level_map, const Thresholds* th, uint8_t* level_map_out,
                int B, float* y, int accumulate, hipStream_t s);

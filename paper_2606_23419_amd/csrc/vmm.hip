@@ -68,7 +68,7 @@ __global__ __launch_bounds__(kVmmThreads) void k_vmm_v0(
         lvl = min((int)lm[(size_t)tok * L.K + k], L.n_levels - 1);
       }
       if (lvl == 0) continue;
-      const int d = L.planes[lvl];
+      const int d = level_planes(L.planes_packed, lvl);
       const int b = d * U;
       const uint8_t* row = codes + ((size_t)t * L.K + k) * L.T;
       uint32_t code[16];
@@ -111,6 +111,8 @@ int launch_vmm(const Layer& L, const void* codes, const void* scales, const void
     int st = check_launch("vmm zero-fill");
     if (st) return st;
   }
+  if (vmm_dot2_supported(L))
+    return launch_vmm_dot2(L, codes, scales, x, level_map, th, level_map_out, B, y, s);
   // about 512 workgroups per token over the whole chip
   int ksplit = (512 + L.tiles - 1) / L.tiles;
   if (ksplit > L.groups) ksplit = L.groups;

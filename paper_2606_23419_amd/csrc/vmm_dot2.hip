@@ -1,0 +1,429 @@
+// Nested-precision decode VMM for 2-bit planes (Sec. 3.3 reconstruction with
+// the midpoint bias; App. C.1 sparse bit-loading), laid out for CDNA4.
+//
+// Work items are plane rows: (channel k, plane j) for j = 1 .. the depth that
+// k's level asks for (for B > 1 tokens, the deepest of the B levels).  A
+// workgroup owns one tile of T = 256*V outputs and `gw` consecutive groups of
+// 128 channels.  Its prologue lists, per group, the plane rows to read and
+// pairs consecutive ones; the main loop streams the pairs.
+//
+// A pair is consumed with v_dot2_f32_f16.  For 16 outputs a lane loads one
+// dword of each plane row (sixteen 2-bit fields); v_perm_b32 puts eight
+// outputs' fields of row 1 in the low half and of row 2 in the high half.  A
+// field c at bit p of a half, OR-ed with the exponent bits E = 33 - 2j - p
+// (fp16 bias 15), reads as the fp16 value 2^(18-2j-p) + c * 2^(8-2j): the
+// field at its code-unit weight 2^(8-2j) plus an offset 2^(10-p) * 2^(8-2j).
+// Fields at p in {4, 6, 8} are used as they lie, the others after a shift of
+// the whole dword (<< 4 or >> 6), so eight fp16 pairs cost eight v_and_or_b32
+// and two shifts.  One dot2 with the pair (x_k1, x_k2) then adds both rows'
+// contributions to the output's fp32 accumulator.  The same dot2 applied to
+// the bare exponent bits of position 4 (fields zero) gives 64 (x_k1 w_1 +
+// x_k2 w_2), the pair's offset at p = 4; each lane group sums it alongside,
+// so its partial sum can drop the offsets before anything is combined.
+// Per group and output,
+//   y_n += s_{g,n} * (acc_n - 2^(4-p(n)) * off_g + beta_g),
+//   off_g  = sum over the group's pairs of 64 (x_k1 w_1 + x_k2 w_2),
+//   beta_g = sum_{k: level > 0} x_k (phi_b - 128)  (midpoint bias, offset),
+// which equals sum_k x_k s (t_k + phi - 128) with t_k the truncated code.
+#include <cstdlib>
+
+#include "grinqh_internal.h"
+
+namespace grinqh {
+
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kWaves = kThreads / 64;
+constexpr int kLaneGroups = kThreads / 16;   // 16 lanes cover one plane row of a tile
+constexpr int kMaxGW = 4;                    // groups per workgroup (B = 1)
+constexpr int max_gw(int nb) { return nb == 1 ? kMaxGW : 2; }   // LDS of the pair lists
+constexpr int kMaxItems = kGroup * 4;        // 128 rows x 4 planes
+constexpr int kMaxPairs = kMaxItems / 2;
+
+typedef _Float16 half2_t __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ float dot2(uint32_t a, uint32_t b, float c) {
+  return __builtin_amdgcn_fdot2(__builtin_bit_cast(half2_t, a), __builtin_bit_cast(half2_t, b), c,
+                                false);
+}
+
+// Number of set predicates in lanes below this one, and in the whole wave.
+__device__ __forceinline__ int lanes_below(bool pred) {
+  const uint64_t m = __ballot(pred);
+  return (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+}
+__device__ __forceinline__ int lanes_total(bool pred) { return (int)__popcll(__ballot(pred)); }
+
+// Make this wave's LDS writes visible to its own later LDS reads.
+__device__ __forceinline__ void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
+  return v;
+}
+
+// Per-pair descriptor: byte offsets of the two plane chunks from the tile
+// base, the fp16x2 exponent bits for field position 4, and one fp16x2
+// coefficient pair per token (0 where that token does not read the plane).
+template <int NB>
+struct Desc {
+  static constexpr int DW = NB == 1 ? 4 : 8;
+};
+
+// Sixteen outputs of one pair: w1/w2 are the two plane rows' dwords.
+template <int NB, int NACC>
+__device__ __forceinline__ void consume_pair(uint32_t w1, uint32_t w2, uint32_t m4,
+                                             const uint32_t (&xp)[NB], float (&acc)[NB][NACC],
+                                             int base) {
+  const uint32_t m6 = m4 - 0x08000800u;   // exponent field - 2 in both halves
+  const uint32_t m8 = m4 - 0x10001000u;   // exponent field - 4
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const uint32_t R = __builtin_amdgcn_perm(w2, w1, h ? 0x07060302u : 0x05040100u);
+    const uint32_t A = R, Bv = R << 4, C = R >> 6;
+    uint32_t f[8];
+    f[0] = (Bv & 0x00300030u) | m4;   // field 0: bits 0-1 moved to 4-5
+    f[1] = (Bv & 0x00C000C0u) | m6;   // field 1: bits 2-3 -> 6-7
+    f[2] = (A & 0x00300030u) | m4;    // field 2: bits 4-5
+    f[3] = (A & 0x00C000C0u) | m6;    // field 3: bits 6-7
+    f[4] = (A & 0x03000300u) | m8;    // field 4: bits 8-9
+    f[5] = (C & 0x00300030u) | m4;    // field 5: bits 10-11 -> 4-5
+    f[6] = (C & 0x00C000C0u) | m6;    // field 6: bits 12-13 -> 6-7
+    f[7] = (C & 0x03000300u) | m8;    // field 7: bits 14-15 -> 8-9
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+#pragma unroll
+      for (int b = 0; b < NB; ++b) acc[b][base + h * 8 + e] = dot2(f[e], xp[b], acc[b][base + h * 8 + e]);
+  }
+}
+
+// 2^(4-p) for the field position p used by output e (mod 8) above: the
+// output's offset relative to the position-4 offset summed per pair.
+__device__ __forceinline__ float offset_factor(int e) {
+  const int m = e & 7;
+  return (m == 4 || m == 7) ? 0.0625f : ((m == 1 || m == 3 || m == 6) ? 0.25f : 1.0f);
+}
+
+__device__ __forceinline__ float phi_minus_offset(int b) {
+  return (b < 8 ? (float)(1 << (7 - b)) : 0.0f) - 128.0f;
+}
+
+template <int V>
+struct Words {
+  uint32_t w[V];
+};
+
+template <int V>
+__device__ __forceinline__ Words<V> load_words(const uint8_t* p) {
+  Words<V> r;
+  if constexpr (V == 1) {
+    r.w[0] = __builtin_nontemporal_load((const uint32_t*)p);
+  } else {
+    typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+    const u32x2 v = __builtin_nontemporal_load((const u32x2*)p);
+    r.w[0] = v.x;
+    r.w[1] = v.y;
+  }
+  return r;
+}
+
+// Sum of a value over the four 16-lane rows of a wave, in every lane.
+// v_permlane32_swap exchanges the upper 32 lanes of its first operand with
+// the lower 32 of its second, and v_permlane16_swap the odd rows of the first
+// with the even rows of the second; both write both registers.  They are
+// written as asm with both registers as in/out operands: the compiler's
+// builtins for them, given one value twice, have been seen to read back the
+// first result in place of the second.  s_nop 1 covers the VALU-write to
+// permlane-read hazard of the copy just before.
+__device__ __forceinline__ float row_sum4(float v) {
+  uint32_t a = __builtin_bit_cast(uint32_t, v), b = a;
+  asm volatile("s_nop 1\n\tv_permlane32_swap_b32 %0, %1" : "+v"(a), "+v"(b));
+  v = __builtin_bit_cast(float, a) + __builtin_bit_cast(float, b);   // rows r and r^2
+  a = __builtin_bit_cast(uint32_t, v);
+  b = a;
+  asm volatile("s_nop 1\n\tv_permlane16_swap_b32 %0, %1" : "+v"(a), "+v"(b));
+  return __builtin_bit_cast(float, a) + __builtin_bit_cast(float, b);  // and r^1
+}
+
+template <int V, int NB, int PB>
+__global__ __launch_bounds__(kThreads) void k_vmm_dot2(
+    const uint8_t* __restrict__ codes, const uint16_t* __restrict__ scales,
+    const uint16_t* __restrict__ x, const uint8_t* __restrict__ lm, float* __restrict__ y,
+    Layer L, int gw, int fused, Thresholds th, uint8_t* __restrict__ lm_out) {
+  constexpr int T = 256 * V;
+  constexpr int NACC = 16 * V;
+  constexpr int DW = Desc<NB>::DW;
+
+  __shared__ __align__(16) uint32_t s_pairs[max_gw(NB)][kMaxPairs][DW];
+  __shared__ int s_npairs[max_gw(NB)];
+  __shared__ float s_beta[max_gw(NB)][NB];
+  __shared__ __align__(16) float s_red[NB][kWaves][T];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int t = blockIdx.x % L.tiles;
+  const int g0 = (blockIdx.x / L.tiles) * gw;
+  const int ng = min(gw, L.groups - g0);
+  const int n_top = L.n_levels - 1;
+  const int lg = tid >> 4, li = tid & 15;
+
+  // the first group's scales load while the prologue runs; later groups'
+  // scales load while the previous group streams
+  uint4 sv[NACC / 8];
+  {
+    const uint16_t* sp = scales + (size_t)g0 * L.N + (size_t)t * T + li * NACC;
+#pragma unroll
+    for (int c = 0; c < NACC / 8; ++c) sv[c] = *(const uint4*)(sp + 8 * c);
+  }
+
+  // ---- prologue: one wave per group.  Lane l grades rows 2l and 2l+1, lists
+  // their plane rows (row 2l first, planes in order) and pairs them in order;
+  // a pair's second slot is empty when the lane's count is odd.  Pair slots
+  // are placed by ballot prefix counts, so the lane writes its descriptors
+  // straight into the group's list.
+  for (int gg = wave; gg < ng; gg += kWaves) {
+    const int g = g0 + gg;
+    const int r0 = 2 * lane;
+    const int k0 = g * kGroup + r0;
+    uint32_t xxs[NB];
+    uint16_t lls[NB];
+    const uint8_t* lmsrc = fused ? (const uint8_t*)x : lm;   // in fused mode the read is ignored
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+      xxs[b] = *(const uint32_t*)(x + (size_t)b * L.K + k0);
+      lls[b] = *(const uint16_t*)(lmsrc + (size_t)b * L.K + k0);
+    }
+    int da[NB], db[NB];
+    int D0 = 0, D1 = 0;
+    float beta[NB];
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+      const float fa = h2f((uint16_t)(xxs[b] & 0xFFFFu)), fb = h2f((uint16_t)(xxs[b] >> 16));
+      int la, lb;
+      if (fused) {
+        la = 0;
+        lb = 0;
+        const float aa = fabsf(fa), ab = fabsf(fb);
+        for (int j = 0; j < th.n; ++j) {
+          la += aa >= th.theta[j] ? 1 : 0;
+          lb += ab >= th.theta[j] ? 1 : 0;
+        }
+        if (lm_out && t == 0)
+          *(uint16_t*)(lm_out + (size_t)b * L.K + k0) = (uint16_t)(la | (lb << 8));
+      } else {
+        la = min((int)(lls[b] & 0xFFu), n_top);
+        lb = min((int)(lls[b] >> 8), n_top);
+      }
+      da[b] = level_planes(L.planes_packed, la);
+      db[b] = level_planes(L.planes_packed, lb);
+      D0 = max(D0, da[b]);
+      D1 = max(D1, db[b]);
+      beta[b] = (la ? fa * phi_minus_offset(2 * da[b]) : 0.0f) +
+                (lb ? fb * phi_minus_offset(2 * db[b]) : 0.0f);
+    }
+    const int cnt = D0 + D1;
+    const int np = (cnt + 1) >> 1;
+    int pos = 0, total = 0;
+#pragma unroll
+    for (int q = 1; q <= 4; ++q) {
+      pos += lanes_below(np >= q);
+      total += lanes_total(np >= q);
+    }
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      if (2 * q >= cnt) break;
+      // items 2q and 2q+1 of the lane: item i is (row r0, plane i+1) below D0,
+      // else (row r0+1, plane i-D0+1)
+      const int ia = 2 * q, ib = 2 * q + 1;
+      const bool has_b = ib < cnt;
+      const int ra = ia < D0 ? 0 : 1, ja = ia < D0 ? ia + 1 : ia - D0 + 1;
+      const int rb = ib < D0 ? 0 : 1, jb = has_b ? (ib < D0 ? ib + 1 : ib - D0 + 1) : ja;
+      const int rbb = has_b ? rb : ra;
+      uint32_t* d = s_pairs[gg][pos + q];
+      d[0] = (uint32_t)((k0 + ra) * T + (ja - 1) * (T / 4));
+      d[1] = (uint32_t)((k0 + rbb) * T + (jb - 1) * (T / 4));
+      d[2] = ((uint32_t)(29 - 2 * ja) << 10) | ((uint32_t)(29 - 2 * jb) << 26);
+#pragma unroll
+      for (int b = 0; b < NB; ++b) {
+        const uint32_t xa = ra ? (xxs[b] >> 16) : (xxs[b] & 0xFFFFu);
+        const uint32_t xb = rb ? (xxs[b] >> 16) : (xxs[b] & 0xFFFFu);
+        const int dA = ra ? db[b] : da[b];
+        const int dB = rb ? db[b] : da[b];
+        const uint32_t c1 = ja <= dA ? xa : 0u;
+        const uint32_t c2 = (has_b && jb <= dB) ? xb : 0u;
+        d[3 + b] = c1 | (c2 << 16);
+      }
+#pragma unroll
+      for (int w = 3 + NB; w < DW; ++w) d[w] = 0u;
+    }
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+      const float bs = wave_sum(beta[b]);
+      if (lane == 0) s_beta[gg][b] = bs;
+    }
+    if (lane == 0) s_npairs[gg] = total;
+  }
+  __syncthreads();
+
+  // ---- main loop: lane group lg takes pairs lg, lg + 16, ... of every group
+  const uint8_t* tile = codes + (size_t)t * L.K * T + li * 4 * V;
+  float yp[NB][NACC];
+#pragma unroll
+  for (int b = 0; b < NB; ++b)
+#pragma unroll
+    for (int e = 0; e < NACC; ++e) yp[b][e] = 0.0f;
+
+  for (int gg = 0; gg < ng; ++gg) {
+    const int np = s_npairs[gg];
+    const int R = (np + kLaneGroups - 1) / kLaneGroups;
+    float acc[NB][NACC], off[NB];
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+      off[b] = 0.0f;
+#pragma unroll
+      for (int e = 0; e < NACC; ++e) acc[b][e] = 0.0f;
+    }
+
+    for (int r = 0; r < R; r += PB) {
+      uint32_t dsc[PB][DW];
+      bool valid[PB];
+      Words<V> w1[PB], w2[PB];
+#pragma unroll
+      for (int q = 0; q < PB; ++q) {
+        const int i = lg + kLaneGroups * (r + q);
+        valid[q] = i < np;
+        const uint32_t* src = s_pairs[gg][valid[q] ? i : 0];
+        const uint4 a = *(const uint4*)src;
+        // an empty slot gets zero coefficients and a finite exponent word
+        // (LDS behind it may hold anything, and 0 * inf would be NaN)
+        dsc[q][0] = a.x; dsc[q][1] = a.y;
+        dsc[q][2] = valid[q] ? a.z : ((27u << 10) | (27u << 26));
+        dsc[q][3] = valid[q] ? a.w : 0u;
+        if constexpr (DW == 8) {
+          const uint4 c = *(const uint4*)(src + 4);
+          dsc[q][4] = valid[q] ? c.x : 0u; dsc[q][5] = valid[q] ? c.y : 0u;
+          dsc[q][6] = valid[q] ? c.z : 0u; dsc[q][7] = c.w;
+        }
+      }
+#pragma unroll
+      for (int q = 0; q < PB; ++q) {
+        if (valid[q]) {
+          w1[q] = load_words<V>(tile + dsc[q][0]);
+          w2[q] = load_words<V>(tile + dsc[q][1]);
+        } else {
+#pragma unroll
+          for (int v = 0; v < V; ++v) w1[q].w[v] = w2[q].w[v] = 0u;
+        }
+      }
+#pragma unroll
+      for (int q = 0; q < PB; ++q) {
+        uint32_t xp[NB];
+#pragma unroll
+        for (int b = 0; b < NB; ++b) {
+          xp[b] = dsc[q][3 + b];
+          off[b] = dot2(dsc[q][2], xp[b], off[b]);
+        }
+#pragma unroll
+        for (int v = 0; v < V; ++v) consume_pair<NB, NACC>(w1[q].w[v], w2[q].w[v], dsc[q][2], xp, acc, 16 * v);
+      }
+    }
+
+    // group epilogue: scale, and (once per output) the offset/bias terms
+    float s[NACC];
+#pragma unroll
+    for (int c = 0; c < NACC / 8; ++c) {
+      const uint4 v = sv[c];
+      const uint32_t ww[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+      for (int h = 0; h < 4; ++h) {
+        s[8 * c + 2 * h] = h2f((uint16_t)(ww[h] & 0xFFFFu));
+        s[8 * c + 2 * h + 1] = h2f((uint16_t)(ww[h] >> 16));
+      }
+    }
+    if (gg + 1 < ng) {
+      const uint16_t* sp = scales + (size_t)(g0 + gg + 1) * L.N + (size_t)t * T + li * NACC;
+#pragma unroll
+      for (int c = 0; c < NACC / 8; ++c) sv[c] = *(const uint4*)(sp + 8 * c);
+    }
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+      const float beta = lg == 0 ? s_beta[gg][b] : 0.0f;
+#pragma unroll
+      for (int e = 0; e < NACC; ++e)
+        yp[b][e] = fmaf(s[e], (acc[b][e] - offset_factor(e) * off[b]) + beta, yp[b][e]);
+    }
+  }
+
+  // ---- reduce: the four lane groups of a wave with lane swaps, the waves
+  // through LDS, then one atomic add per output
+#pragma unroll
+  for (int b = 0; b < NB; ++b)
+#pragma unroll
+    for (int e = 0; e < NACC; ++e) yp[b][e] = row_sum4(yp[b][e]);
+  if (lane < 16) {
+#pragma unroll
+    for (int b = 0; b < NB; ++b)
+#pragma unroll
+      for (int c = 0; c < NACC / 4; ++c)
+        *(float4*)&s_red[b][wave][li * NACC + 4 * c] =
+            make_float4(yp[b][4 * c], yp[b][4 * c + 1], yp[b][4 * c + 2], yp[b][4 * c + 3]);
+  }
+  __syncthreads();
+  for (int i = tid; i < NB * T; i += kThreads) {
+    const int b = i / T, o = i % T;
+    float v = 0.0f;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) v += s_red[b][w][o];
+    atomicAdd(&y[(size_t)b * L.N + (size_t)t * T + o], v);
+  }
+}
+
+template <int V, int NB>
+void launch_one(dim3 grid, hipStream_t s, const void* codes, const void* scales, const void* x,
+                const uint8_t* lm, float* y, const Layer& L, int gw, int fused,
+                const Thresholds& th, uint8_t* lm_out) {
+  constexpr int PB = (NB == 1 && V == 1) ? 8 : 4;
+  hipLaunchKernelGGL((k_vmm_dot2<V, NB, PB>), grid, dim3(kThreads), 0, s, (const uint8_t*)codes,
+                     (const uint16_t*)scales, (const uint16_t*)x, lm, y, L, gw, fused, th, lm_out);
+}
+
+}  // namespace
+
+bool vmm_dot2_supported(const Layer& L) { return L.u == 2 && (L.T == 256 || L.T == 512); }
+
+int vmm_dot2_groups_per_wg(const Layer& L) {
+  const char* env = getenv("GRINQH_VMM_GW");
+  if (env) {
+    const int v = atoi(env);
+    if (v >= 1 && v <= kMaxGW) return v;
+  }
+  const long wgs = (long)L.tiles * L.groups;
+  int gw = (int)((wgs + 256) / 512);
+  return gw < 1 ? 1 : (gw > kMaxGW ? kMaxGW : gw);
+}
+
+int launch_vmm_dot2(const Layer& L, const void* codes, const void* scales, const void* x,
+                    const uint8_t* level_map, const Thresholds* th, uint8_t* level_map_out,
+                    int B, float* y, hipStream_t s) {
+  const int gw = min(vmm_dot2_groups_per_wg(L), max_gw(B));
+  const dim3 grid((unsigned)(L.tiles * ((L.groups + gw - 1) / gw)));
+  Thresholds none{};
+  const Thresholds& tt = th ? *th : none;
+  const int fused = th != nullptr;
+#define GRINQH_DOT2_CASE(VV, NN)                                                                \
+  if (L.T == 256 * VV && B == NN) {                                                            \
+    launch_one<VV, NN>(grid, s, codes, scales, x, level_map, y, L, gw, fused, tt, level_map_out); \
+    return check_launch("vmm (dot2)");                                                         \
+  }
+  GRINQH_DOT2_CASE(1, 1) GRINQH_DOT2_CASE(1, 2) GRINQH_DOT2_CASE(1, 3) GRINQH_DOT2_CASE(1, 4)
+  GRINQH_DOT2_CASE(2, 1) GRINQH_DOT2_CASE(2, 2) GRINQH_DOT2_CASE(2, 3) GRINQH_DOT2_CASE(2, 4)
+#undef GRINQH_DOT2_CASE
+  return fail(GRINQH_EUNSUPPORTED, "dot2 VMM: no kernel for tile %d, B=%d", L.T, B);
+}
+
+}  // namespace grinqh

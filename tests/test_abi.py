@@ -129,8 +129,8 @@ def test_assign_validation(g):
     assert A(ctypes.byref(d), 1, FAKE, 1, None, _cn([-1, 1, 1, 255]), FAKE, None, 0, None) == -1
     assert A(ctypes.byref(d), 1, FAKE, 1, _th([1, 2, 3]), _cn([64, 64, 64, 64]), FAKE, None, 0, None) == -1
     assert A(ctypes.byref(d), 5, FAKE, 1, None, None, FAKE, None, 0, None) == -1
-    big = g.make_desc(128 * 1024, 512, (0, 8))
-    assert A(ctypes.byref(big), 1, FAKE, 1, None, _cn([0, 128 * 1024]), FAKE, None, 0, None) == -2
+    big = g.make_desc(128 * 129, 512, (0, 8))
+    assert A(ctypes.byref(big), 1, FAKE, 1, None, _cn([0, 128 * 129]), FAKE, None, 0, None) == -2
 
 
 def test_vmm_validation(g):

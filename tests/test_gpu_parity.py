@@ -279,3 +279,35 @@ def test_full_size_pack_and_sampled_vmm(g, torch, name, K, N, levels, xkind):
         # sampled outputs against the oracle, and the whole vector's scale
         assert normwise(y[:, rows], ref) <= TOL, (name, p)
         assert np.all(np.isfinite(y))
+
+
+@pytest.mark.parametrize("gw", ["1", "2", "3", "4"])
+@pytest.mark.parametrize("tile_n", [256, 512])
+def test_vmm_groups_per_workgroup(g, torch, gw, tile_n, monkeypatch):
+    # K = 1152 is 9 groups: every gw > 1 leaves a ragged last workgroup
+    monkeypatch.setenv("GRINQH_VMM_GW", gw)
+    levels = (0, 2, 4, 6, 8)
+    K, N = 1152, 1024
+    L = Layer(g, torch, K, N, levels, cfg=64, tile_n=tile_n)
+    rng = np.random.default_rng(64)
+    for B in (1, 2, 4):
+        x = inputs.activations_t3(K, B, 64, B)
+        lm = rng.integers(0, 5, size=(B, K)).astype(np.uint8)
+        y, ref = _vmm_case(g, torch, L, x, lm)
+        assert normwise(y, ref) <= TOL, (gw, tile_n, B, normwise(y, ref))
+
+
+def test_vmm_precision_margin(g, torch):
+    # the contract is 1e-3; the fp32 accumulation should sit far below it
+    levels = (0, 2, 4, 6, 8)
+    K, N = 4096, 1024
+    L = Layer(g, torch, K, N, levels, cfg=65, tile_n=256)
+    x = inputs.activations_t3(K, 2, 65)
+    worst = 0.0
+    for p in inputs.BUDGETS[levels].values():
+        counts = g.grinqh_topk_counts(K, p)
+        lm = _host(g.grinqh_assign(L.desc, _dev(torch, x), g.GRINQH_ASSIGN_TOPK, counts=counts))
+        y, ref = _vmm_case(g, torch, L, x, lm)
+        worst = max(worst, normwise(y, ref))
+    print(f"worst normwise error {worst:.2e}")
+    assert worst <= 1e-4
