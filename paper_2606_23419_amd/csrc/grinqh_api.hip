@@ -54,9 +54,18 @@ static int resolve(const grinqh_layer_desc* d, Layer* L, grinqh_layer_desc* out)
       return fail(GRINQH_EINVAL, "level %d has %d bits, not a multiple of plane_bits=%d", i, d->level_bits[i], u);
   int T = d->tile_n;
   if (T == 0) {
-    const int pref[] = {512, 1024, 2048, 256};
-    for (int c : pref) {
-      if (c * u >= 512 && d->N % c == 0) { T = c; break; }
+    // Auto: the widest tile (fewer, longer rows per workgroup) that still
+    // leaves at least 256 (tile, group) work units for 256 CUs; if none does,
+    // the tile giving the most units.
+    const long groups = d->K / kGroup;
+    const int cand[] = {1024, 512, 256};
+    for (int c : cand) {
+      if (c * u >= 512 && d->N % c == 0 && (long)(d->N / c) * groups >= 256) { T = c; break; }
+    }
+    if (T == 0) {
+      for (int c : {256, 512, 1024, 2048}) {
+        if (c * u >= 512 && d->N % c == 0) { T = c; break; }
+      }
     }
     if (T == 0) return fail(GRINQH_EUNSUPPORTED, "N=%d has no supported tile width for plane_bits=%d", d->N, u);
   } else {

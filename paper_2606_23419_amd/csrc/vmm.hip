@@ -111,7 +111,7 @@ int launch_vmm(const Layer& L, const void* codes, const void* scales, const void
     int st = check_launch("vmm zero-fill");
     if (st) return st;
   }
-  if (vmm_dot2_supported(L))
+  if (vmm_dot2_supported(L) && !(L.T == 1024 && B > 2))
     return launch_vmm_dot2(L, codes, scales, x, level_map, th, level_map_out, B, y, s);
   // about 512 workgroups per token over the whole chip
   int ksplit = (512 + L.tiles - 1) / L.tiles;

@@ -33,9 +33,6 @@ namespace grinqh {
 
 namespace {
 
-constexpr int kThreads = 256;
-constexpr int kWaves = kThreads / 64;
-constexpr int kLaneGroups = kThreads / 16;   // 16 lanes cover one plane row of a tile
 constexpr int kMaxGW = 4;                    // groups per workgroup (B = 1)
 constexpr int max_gw(int nb) { return nb == 1 ? kMaxGW : 2; }   // LDS of the pair lists
 constexpr int kMaxItems = kGroup * 4;        // 128 rows x 4 planes
@@ -151,18 +148,53 @@ __device__ __forceinline__ float row_sum4(float v) {
   return __builtin_bit_cast(float, a) + __builtin_bit_cast(float, b);  // and r^1
 }
 
-template <int V, int NB, int PB>
+// Rotate right by n lanes inside each 16-lane row (DPP row_ror).
+template <int n>
+__device__ __forceinline__ float row_ror(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v),
+                                                               0x120 + n, 0xF, 0xF, false));
+}
+
+// Sum over the whole wave, in every lane: row sums by rotation, then rows.
+__device__ __forceinline__ float wave_sum_dpp(float v) {
+  v += row_ror<8>(v);
+  v += row_ror<4>(v);
+  v += row_ror<2>(v);
+  v += row_ror<1>(v);
+  return row_sum4(v);
+}
+
+// Sum over the lane groups of a wave that hold the same outputs: LPR lanes
+// cover a plane row, so 64 / LPR lane groups share each output.
+template <int LPR>
+__device__ __forceinline__ float lane_group_sum(float v) {
+  if constexpr (LPR == 16) {
+    return row_sum4(v);
+  } else if constexpr (LPR == 32) {
+    uint32_t a = __builtin_bit_cast(uint32_t, v), b = a;
+    asm volatile("s_nop 1\n\tv_permlane32_swap_b32 %0, %1" : "+v"(a), "+v"(b));
+    return __builtin_bit_cast(float, a) + __builtin_bit_cast(float, b);
+  } else {
+    return v;
+  }
+}
+
+template <int V, int LPR, int NB, int PB, int kThreads>
 __global__ __launch_bounds__(kThreads) void k_vmm_dot2(
     const uint8_t* __restrict__ codes, const uint16_t* __restrict__ scales,
     const uint16_t* __restrict__ x, const uint8_t* __restrict__ lm, float* __restrict__ y,
     Layer L, int gw, int fused, Thresholds th, uint8_t* __restrict__ lm_out) {
-  constexpr int T = 256 * V;
-  constexpr int NACC = 16 * V;
+  constexpr int T = LPR * 16 * V;        // outputs of the tile
+  constexpr int NACC = 16 * V;           // outputs per lane
+  constexpr int kLaneGroups = kThreads / LPR;
+  constexpr int kWaves = kThreads / 64;
   constexpr int DW = Desc<NB>::DW;
 
   __shared__ __align__(16) uint32_t s_pairs[max_gw(NB)][kMaxPairs][DW];
+  __shared__ __align__(16) uint32_t s_empty[kThreads / LPR * PB][DW];   // one all-empty batch
   __shared__ int s_npairs[max_gw(NB)];
   __shared__ float s_beta[max_gw(NB)][NB];
+  __shared__ __align__(16) uint16_t s_scale[max_gw(NB)][T];
   __shared__ __align__(16) float s_red[NB][kWaves][T];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -170,16 +202,8 @@ __global__ __launch_bounds__(kThreads) void k_vmm_dot2(
   const int g0 = (blockIdx.x / L.tiles) * gw;
   const int ng = min(gw, L.groups - g0);
   const int n_top = L.n_levels - 1;
-  const int lg = tid >> 4, li = tid & 15;
+  const int lg = tid / LPR, li = tid % LPR;
 
-  // the first group's scales load while the prologue runs; later groups'
-  // scales load while the previous group streams
-  uint4 sv[NACC / 8];
-  {
-    const uint16_t* sp = scales + (size_t)g0 * L.N + (size_t)t * T + li * NACC;
-#pragma unroll
-    for (int c = 0; c < NACC / 8; ++c) sv[c] = *(const uint4*)(sp + 8 * c);
-  }
 
   // ---- prologue: one wave per group.  Lane l grades rows 2l and 2l+1, lists
   // their plane rows (row 2l first, planes in order) and pairs them in order;
@@ -190,6 +214,17 @@ __global__ __launch_bounds__(kThreads) void k_vmm_dot2(
     const int g = g0 + gg;
     const int r0 = 2 * lane;
     const int k0 = g * kGroup + r0;
+    // this group's scales for the tile go to LDS: T fp16 = 64 lanes x 4V halves
+    {
+      constexpr int H = T / 64;   // halves per lane: 4, 8 or 16
+      const uint16_t* sp = scales + (size_t)g * L.N + (size_t)t * T + lane * H;
+      if constexpr (H == 4) {
+        *(uint2*)&s_scale[gg][lane * H] = *(const uint2*)sp;
+      } else {
+#pragma unroll
+        for (int c = 0; c < H / 8; ++c) *(uint4*)&s_scale[gg][lane * H + 8 * c] = *(const uint4*)(sp + 8 * c);
+      }
+    }
     uint32_t xxs[NB];
     uint16_t lls[NB];
     const uint8_t* lmsrc = fused ? (const uint8_t*)x : lm;   // in fused mode the read is ignored
@@ -263,100 +298,160 @@ __global__ __launch_bounds__(kThreads) void k_vmm_dot2(
     }
 #pragma unroll
     for (int b = 0; b < NB; ++b) {
-      const float bs = wave_sum(beta[b]);
+      const float bs = wave_sum_dpp(beta[b]);
       if (lane == 0) s_beta[gg][b] = bs;
+    }
+    // pad the list to whole batches with empty descriptors (zero coefficients,
+    // offset 0, a finite exponent word), so the main loop needs no bounds tests
+    {
+      // an empty list still gets one batch (its group epilogue runs), so it
+      // is padded to kSlots, never to 0
+      constexpr int kSlots = kThreads / LPR * PB;
+      const int padded = total > 0 ? (total + kSlots - 1) / kSlots * kSlots : kSlots;
+      for (int i = total + lane; i < padded; i += 64) {
+        uint32_t* d = s_pairs[gg][i];
+        d[0] = 0u;
+        d[1] = 0u;
+        d[2] = (27u << 10) | (27u << 26);
+#pragma unroll
+        for (int w = 3; w < DW; ++w) d[w] = 0u;
+      }
     }
     if (lane == 0) s_npairs[gg] = total;
   }
+  for (int i = tid; i < (kThreads / LPR * PB) * DW; i += kThreads)
+    (&s_empty[0][0])[i] = (i % DW == 2) ? ((27u << 10) | (27u << 26)) : 0u;
   __syncthreads();
 
-  // ---- main loop: lane group lg takes pairs lg, lg + 16, ... of every group
+  // ---- main loop: lane group lg takes pairs lg, lg + 16, ... of every group.
+  // The (group, batch) sequence is walked with two register sets: the loads
+  // of the next batch are in flight while the current one is consumed, across
+  // group boundaries too.  A group with no pairs still gets one (empty) batch
+  // so its epilogue runs and the scale prefetch advances.
   const uint8_t* tile = codes + (size_t)t * L.K * T + li * 4 * V;
-  float yp[NB][NACC];
+  float yp[NB][NACC], acc[NB][NACC], off[NB];
 #pragma unroll
-  for (int b = 0; b < NB; ++b)
+  for (int b = 0; b < NB; ++b) {
+    off[b] = 0.0f;
 #pragma unroll
-    for (int e = 0; e < NACC; ++e) yp[b][e] = 0.0f;
+    for (int e = 0; e < NACC; ++e) yp[b][e] = acc[b][e] = 0.0f;
+  }
 
-  for (int gg = 0; gg < ng; ++gg) {
-    const int np = s_npairs[gg];
-    const int R = (np + kLaneGroups - 1) / kLaneGroups;
-    float acc[NB][NACC], off[NB];
+  // A batch in flight keeps what the math needs: per pair the exponent word,
+  // the coefficient pairs and the two loaded words (offsets are used at fetch)
+  struct Batch {
+    uint32_t m4[PB];
+    uint32_t xp[PB][NB];
+    uint32_t w1[PB][V], w2[PB][V];
+  };
+  // flattened batch sequence: group gg owns batches [bstart[gg], bstart[gg+1])
+  int bstart[max_gw(NB) + 1];
+  bstart[0] = 0;
 #pragma unroll
-    for (int b = 0; b < NB; ++b) {
-      off[b] = 0.0f;
+  for (int gg = 0; gg < max_gw(NB); ++gg) {
+    int r = gg < ng ? (s_npairs[gg] + kLaneGroups * PB - 1) / (kLaneGroups * PB) : 0;
+    if (gg < ng && r == 0) r = 1;   // an empty group still gets its epilogue
+    bstart[gg + 1] = bstart[gg] + r;
+  }
+  const int nbt = bstart[max_gw(NB)];
+  auto group_of = [&](int b) {
+    int gg = 0;
 #pragma unroll
-      for (int e = 0; e < NACC; ++e) acc[b][e] = 0.0f;
+    for (int k = 1; k < max_gw(NB); ++k) gg += (b >= bstart[k]) ? 1 : 0;
+    return gg;
+  };
+  // Issue batch b (b >= nbt reads the all-empty batch).  There is no test
+  // and no branch: each group's list is padded to whole batches with empty
+  // descriptors (offset 0, the tile's first row, cached and in bounds; zero
+  // coefficients; a finite exponent word, so masked fields stay finite and
+  // cancel).  With straight-line loads the compiler counts them exactly and
+  // waits only for the batch being consumed.
+  auto fetch = [&](Batch& B, int b) {
+    const int gg = group_of(b);
+    const int r0 = (b - bstart[gg]) * PB;
+    const uint32_t* base = b < nbt ? s_pairs[gg][r0 * kLaneGroups] : s_empty[0];
+#pragma unroll
+    for (int q = 0; q < PB; ++q) {
+      const uint32_t* src = base + (lg + kLaneGroups * q) * DW;
+      const uint4 a = *(const uint4*)src;
+      B.m4[q] = a.z;
+      if constexpr (DW == 4) {
+        B.xp[q][0] = a.w;
+      } else {
+        const uint4 c = *(const uint4*)(src + 4);
+        const uint32_t cw[5] = {a.w, c.x, c.y, c.z, c.w};
+#pragma unroll
+        for (int b = 0; b < NB; ++b) B.xp[q][b] = cw[b];
+      }
+      const Words<V> u1 = load_words<V>(tile + a.x);
+      const Words<V> u2 = load_words<V>(tile + a.y);
+#pragma unroll
+      for (int v = 0; v < V; ++v) {
+        B.w1[q][v] = u1.w[v];
+        B.w2[q][v] = u2.w[v];
+      }
     }
-
-    for (int r = 0; r < R; r += PB) {
-      uint32_t dsc[PB][DW];
-      bool valid[PB];
-      Words<V> w1[PB], w2[PB];
+  };
+  auto consume = [&](const Batch& B) {
 #pragma unroll
-      for (int q = 0; q < PB; ++q) {
-        const int i = lg + kLaneGroups * (r + q);
-        valid[q] = i < np;
-        const uint32_t* src = s_pairs[gg][valid[q] ? i : 0];
-        const uint4 a = *(const uint4*)src;
-        // an empty slot gets zero coefficients and a finite exponent word
-        // (LDS behind it may hold anything, and 0 * inf would be NaN)
-        dsc[q][0] = a.x; dsc[q][1] = a.y;
-        dsc[q][2] = valid[q] ? a.z : ((27u << 10) | (27u << 26));
-        dsc[q][3] = valid[q] ? a.w : 0u;
-        if constexpr (DW == 8) {
-          const uint4 c = *(const uint4*)(src + 4);
-          dsc[q][4] = valid[q] ? c.x : 0u; dsc[q][5] = valid[q] ? c.y : 0u;
-          dsc[q][6] = valid[q] ? c.z : 0u; dsc[q][7] = c.w;
-        }
-      }
+    for (int q = 0; q < PB; ++q) {
 #pragma unroll
-      for (int q = 0; q < PB; ++q) {
-        if (valid[q]) {
-          w1[q] = load_words<V>(tile + dsc[q][0]);
-          w2[q] = load_words<V>(tile + dsc[q][1]);
-        } else {
+      for (int b = 0; b < NB; ++b) off[b] = dot2(B.m4[q], B.xp[q][b], off[b]);
 #pragma unroll
-          for (int v = 0; v < V; ++v) w1[q].w[v] = w2[q].w[v] = 0u;
-        }
-      }
-#pragma unroll
-      for (int q = 0; q < PB; ++q) {
-        uint32_t xp[NB];
-#pragma unroll
-        for (int b = 0; b < NB; ++b) {
-          xp[b] = dsc[q][3 + b];
-          off[b] = dot2(dsc[q][2], xp[b], off[b]);
-        }
-#pragma unroll
-        for (int v = 0; v < V; ++v) consume_pair<NB, NACC>(w1[q].w[v], w2[q].w[v], dsc[q][2], xp, acc, 16 * v);
-      }
+      for (int v = 0; v < V; ++v)
+        consume_pair<NB, NACC>(B.w1[q][v], B.w2[q][v], B.m4[q], B.xp[q], acc, 16 * v);
     }
-
-    // group epilogue: scale, and (once per output) the offset/bias terms
-    float s[NACC];
+  };
+  // group epilogue (no global loads): scale from LDS, bias once per output
+  auto finish_group = [&](int gg) {
+    float sc[NACC];
 #pragma unroll
     for (int c = 0; c < NACC / 8; ++c) {
-      const uint4 v = sv[c];
+      const uint4 v = *(const uint4*)&s_scale[gg][li * NACC + 8 * c];
       const uint32_t ww[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
       for (int h = 0; h < 4; ++h) {
-        s[8 * c + 2 * h] = h2f((uint16_t)(ww[h] & 0xFFFFu));
-        s[8 * c + 2 * h + 1] = h2f((uint16_t)(ww[h] >> 16));
+        sc[8 * c + 2 * h] = h2f((uint16_t)(ww[h] & 0xFFFFu));
+        sc[8 * c + 2 * h + 1] = h2f((uint16_t)(ww[h] >> 16));
       }
-    }
-    if (gg + 1 < ng) {
-      const uint16_t* sp = scales + (size_t)(g0 + gg + 1) * L.N + (size_t)t * T + li * NACC;
-#pragma unroll
-      for (int c = 0; c < NACC / 8; ++c) sv[c] = *(const uint4*)(sp + 8 * c);
     }
 #pragma unroll
     for (int b = 0; b < NB; ++b) {
       const float beta = lg == 0 ? s_beta[gg][b] : 0.0f;
 #pragma unroll
-      for (int e = 0; e < NACC; ++e)
-        yp[b][e] = fmaf(s[e], (acc[b][e] - offset_factor(e) * off[b]) + beta, yp[b][e]);
+      for (int e = 0; e < NACC; ++e) {
+        yp[b][e] = fmaf(sc[e], (acc[b][e] - offset_factor(e) * off[b]) + beta, yp[b][e]);
+        acc[b][e] = 0.0f;
+      }
+      off[b] = 0.0f;
     }
+  };
+  auto after = [&](int b) {   // close the group whose last batch b was
+    const int gg = group_of(b);
+    if (b + 1 == bstart[gg + 1]) finish_group(gg);
+  };
+
+  // four register sets: batches b+1 .. b+3 are in flight while b is consumed
+  Batch R0, R1, R2, R3;
+  fetch(R0, 0);
+  fetch(R1, 1);
+  fetch(R2, 2);
+  for (int b = 0; b < nbt; b += 4) {
+    fetch(R3, b + 3);
+    consume(R0);
+    after(b);
+    if (b + 1 >= nbt) break;
+    fetch(R0, b + 4);
+    consume(R1);
+    after(b + 1);
+    if (b + 2 >= nbt) break;
+    fetch(R1, b + 5);
+    consume(R2);
+    after(b + 2);
+    if (b + 3 >= nbt) break;
+    fetch(R2, b + 6);
+    consume(R3);
+    after(b + 3);
   }
 
   // ---- reduce: the four lane groups of a wave with lane swaps, the waves
@@ -364,8 +459,8 @@ __global__ __launch_bounds__(kThreads) void k_vmm_dot2(
 #pragma unroll
   for (int b = 0; b < NB; ++b)
 #pragma unroll
-    for (int e = 0; e < NACC; ++e) yp[b][e] = row_sum4(yp[b][e]);
-  if (lane < 16) {
+    for (int e = 0; e < NACC; ++e) yp[b][e] = lane_group_sum<LPR>(yp[b][e]);
+  if (lane < LPR) {
 #pragma unroll
     for (int b = 0; b < NB; ++b)
 #pragma unroll
@@ -383,18 +478,23 @@ __global__ __launch_bounds__(kThreads) void k_vmm_dot2(
   }
 }
 
-template <int V, int NB>
+template <int V, int LPR, int NB, int NT>
 void launch_one(dim3 grid, hipStream_t s, const void* codes, const void* scales, const void* x,
                 const uint8_t* lm, float* y, const Layer& L, int gw, int fused,
                 const Thresholds& th, uint8_t* lm_out) {
-  constexpr int PB = (NB == 1 && V == 1) ? 8 : 4;
-  hipLaunchKernelGGL((k_vmm_dot2<V, NB, PB>), grid, dim3(kThreads), 0, s, (const uint8_t*)codes,
+  constexpr int PB = (V == 1 && NB <= 2) ? 4 : 2;   // pairs per batch; four batches in flight
+  hipLaunchKernelGGL((k_vmm_dot2<V, LPR, NB, PB, NT>), grid, dim3(NT), 0, s, (const uint8_t*)codes,
                      (const uint16_t*)scales, (const uint16_t*)x, lm, y, L, gw, fused, th, lm_out);
 }
 
 }  // namespace
 
-bool vmm_dot2_supported(const Layer& L) { return L.u == 2 && (L.T == 256 || L.T == 512); }
+// Tiles of 256, 512 or 1024 outputs: one dword (16 outputs) per lane and
+// plane row, so 16, 32 or 64 lanes cover a plane row.  B > 2 keeps the tile
+// at 512 or below (LDS of the cross-wave reduction).
+bool vmm_dot2_supported(const Layer& L) {
+  return L.u == 2 && (L.T == 256 || L.T == 512 || L.T == 1024);
+}
 
 int vmm_dot2_groups_per_wg(const Layer& L) {
   const char* env = getenv("GRINQH_VMM_GW");
@@ -402,8 +502,9 @@ int vmm_dot2_groups_per_wg(const Layer& L) {
     const int v = atoi(env);
     if (v >= 1 && v <= kMaxGW) return v;
   }
-  const long wgs = (long)L.tiles * L.groups;
-  int gw = (int)((wgs + 256) / 512);
+  // about two workgroups per CU when the layer has that many (tile, group) units
+  const long units = (long)L.tiles * L.groups;
+  int gw = (int)(units / 512);
   return gw < 1 ? 1 : (gw > kMaxGW ? kMaxGW : gw);
 }
 
@@ -415,13 +516,22 @@ int launch_vmm_dot2(const Layer& L, const void* codes, const void* scales, const
   Thresholds none{};
   const Thresholds& tt = th ? *th : none;
   const int fused = th != nullptr;
-#define GRINQH_DOT2_CASE(VV, NN)                                                                \
-  if (L.T == 256 * VV && B == NN) {                                                            \
-    launch_one<VV, NN>(grid, s, codes, scales, x, level_map, y, L, gw, fused, tt, level_map_out); \
-    return check_launch("vmm (dot2)");                                                         \
+  const char* env_nt = getenv("GRINQH_VMM_THREADS");
+  const int nt = (env_nt && atoi(env_nt) == 512 && B == 1) ? 512 : 256;
+  if (nt == 512) {
+    if (L.T == 256) launch_one<1, 16, 1, 512>(grid, s, codes, scales, x, level_map, y, L, gw, fused, tt, level_map_out);
+    else if (L.T == 512) launch_one<1, 32, 1, 512>(grid, s, codes, scales, x, level_map, y, L, gw, fused, tt, level_map_out);
+    else launch_one<1, 64, 1, 512>(grid, s, codes, scales, x, level_map, y, L, gw, fused, tt, level_map_out);
+    return check_launch("vmm (dot2)");
   }
-  GRINQH_DOT2_CASE(1, 1) GRINQH_DOT2_CASE(1, 2) GRINQH_DOT2_CASE(1, 3) GRINQH_DOT2_CASE(1, 4)
-  GRINQH_DOT2_CASE(2, 1) GRINQH_DOT2_CASE(2, 2) GRINQH_DOT2_CASE(2, 3) GRINQH_DOT2_CASE(2, 4)
+#define GRINQH_DOT2_CASE(TT, LL, NN)                                                              \
+  if (L.T == TT && B == NN) {                                                                    \
+    launch_one<1, LL, NN, 256>(grid, s, codes, scales, x, level_map, y, L, gw, fused, tt, level_map_out); \
+    return check_launch("vmm (dot2)");                                                           \
+  }
+  GRINQH_DOT2_CASE(256, 16, 1) GRINQH_DOT2_CASE(256, 16, 2) GRINQH_DOT2_CASE(256, 16, 3) GRINQH_DOT2_CASE(256, 16, 4)
+  GRINQH_DOT2_CASE(512, 32, 1) GRINQH_DOT2_CASE(512, 32, 2) GRINQH_DOT2_CASE(512, 32, 3) GRINQH_DOT2_CASE(512, 32, 4)
+  GRINQH_DOT2_CASE(1024, 64, 1) GRINQH_DOT2_CASE(1024, 64, 2)
 #undef GRINQH_DOT2_CASE
   return fail(GRINQH_EUNSUPPORTED, "dot2 VMM: no kernel for tile %d, B=%d", L.T, B);
 }

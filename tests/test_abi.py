@@ -36,8 +36,15 @@ def test_desc_struct_layout_matches_header(g):
 
 
 def test_resolve_auto_fields(g):
+    # widest tile leaving >= 256 (tile, group) units, else the most units
     r = g.grinqh_resolve_desc(g.make_desc(4096, 4096, (0, 2, 4, 6, 8)))
     assert (r.plane_bits, r.tile_n) == (2, 512)
+    r = g.grinqh_resolve_desc(g.make_desc(4096, 14336, (0, 2, 4, 6, 8)))
+    assert r.tile_n == 1024
+    r = g.grinqh_resolve_desc(g.make_desc(14336, 4096, (0, 2, 4, 6, 8)))
+    assert r.tile_n == 1024
+    r = g.grinqh_resolve_desc(g.make_desc(4096, 1024, (0, 2, 4, 6, 8)))
+    assert r.tile_n == 256
     r = g.grinqh_resolve_desc(g.make_desc(4096, 6144, (0, 2, 3, 4, 8)))
     assert (r.plane_bits, r.tile_n) == (1, 512)
     r = g.grinqh_resolve_desc(g.make_desc(1024, 1024, (0, 2, 4, 8), tile_n=256))

@@ -157,7 +157,8 @@ def _vmm_case(g, torch, L, x, lm):
 
 @pytest.mark.parametrize("K,N,levels,tile_n", [
     (128, 512, (0, 2, 4, 8), 0), (640, 1024, (0, 2, 4, 6, 8), 256), (1024, 1024, (0, 2, 4, 8), 0),
-    (384, 2048, (0, 2, 3, 4, 8), 0), (896, 2048, (0, 2, 4, 6, 8), 1024), (256, 2048, (0, 2, 4, 8), 2048)])
+    (384, 2048, (0, 2, 3, 4, 8), 0), (896, 2048, (0, 2, 4, 6, 8), 1024), (256, 2048, (0, 2, 4, 8), 2048),
+    (640, 3072, (0, 2, 4, 6, 8), 1024)])
 @pytest.mark.parametrize("B", [1, 2, 4])
 def test_vmm_topk_parity(g, torch, K, N, levels, tile_n, B):
     L = Layer(g, torch, K, N, levels, tile_n=tile_n)
@@ -281,11 +282,13 @@ def test_full_size_pack_and_sampled_vmm(g, torch, name, K, N, levels, xkind):
         assert np.all(np.isfinite(y))
 
 
+@pytest.mark.parametrize("threads", ["256", "512"])
 @pytest.mark.parametrize("gw", ["1", "2", "3", "4"])
-@pytest.mark.parametrize("tile_n", [256, 512])
-def test_vmm_groups_per_workgroup(g, torch, gw, tile_n, monkeypatch):
+@pytest.mark.parametrize("tile_n", [256, 512, 1024])
+def test_vmm_groups_per_workgroup(g, torch, gw, tile_n, threads, monkeypatch):
     # K = 1152 is 9 groups: every gw > 1 leaves a ragged last workgroup
     monkeypatch.setenv("GRINQH_VMM_GW", gw)
+    monkeypatch.setenv("GRINQH_VMM_THREADS", threads)
     levels = (0, 2, 4, 6, 8)
     K, N = 1152, 1024
     L = Layer(g, torch, K, N, levels, cfg=64, tile_n=tile_n)
@@ -311,3 +314,22 @@ def test_vmm_precision_margin(g, torch):
         worst = max(worst, normwise(y, ref))
     print(f"worst normwise error {worst:.2e}")
     assert worst <= 1e-4
+
+
+@pytest.mark.parametrize("tile_n", [256, 512, 1024])
+@pytest.mark.parametrize("gw", ["1", "2", "4"])
+def test_vmm_groups_with_no_active_channel(g, torch, tile_n, gw, monkeypatch):
+    # groups whose channels are all skipped, next to active ones in the same
+    # workgroup: such a group has no plane rows to read but still runs its
+    # epilogue (regression: its padding once left the batch unwritten)
+    monkeypatch.setenv("GRINQH_VMM_GW", gw)
+    levels = (0, 2, 4, 6, 8)
+    K, N = 1024, 1024
+    L = Layer(g, torch, K, N, levels, cfg=66, tile_n=tile_n)
+    rng = np.random.default_rng(66)
+    lm = rng.integers(0, 5, size=(1, K)).astype(np.uint8)
+    lm[0, 128:384] = 0          # groups 1 and 2 fully skipped
+    lm[0, 896:] = 0             # group 7 fully skipped
+    x = inputs.activations_t3(K, 1, 66)
+    y, ref = _vmm_case(g, torch, L, x, lm)
+    assert normwise(y, ref) <= TOL
