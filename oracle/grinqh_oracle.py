@@ -24,8 +24,7 @@ in numpy with float64 wherever floating point is involved, following the paper
 6. the packed nested layout, written from the layout definition below, so the
    GPU packer's bytes can be compared byte for byte.
 
-Readings taken where the paper is silent or inconsistent (each is also listed
-in DESIGN.md):
+Readings taken where the paper is silent or inconsistent:
 
 * R1  phi at b = b_max is 0: no bits are dropped, so there is no floor to undo.
 * R2  level 0 contributes exactly 0 (skip), not s*phi + z.
