@@ -31,6 +31,10 @@ from synth import inputs  # noqa: E402
 
 HBM_PEAK_GBS = 8000.0
 MALL_ROTATE_BYTES = 512 << 20
+PROFILES = os.path.join(ROOT, "profiles")
+# sources whose change invalidates a stored traffic measurement of the VMM kernel
+VMM_SOURCES = ("paper_2606_23419_amd/csrc/vmm_dot2.hip", "paper_2606_23419_amd/csrc/vmm.hip",
+               "paper_2606_23419_amd/csrc/grinqh_internal.h")
 
 WORKLOADS = {
     # name: (config id, layers [(name, K, N, input id)], level set, budget)
@@ -46,6 +50,50 @@ WORKLOADS = {
 }
 
 
+def vmm_source_sha() -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for rel in VMM_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def stored_traffic(workload: str, budget: int):
+    """HBM bytes per VMM launch from the committed rocprofv3 FETCH_SIZE /
+    WRITE_SIZE summary of this workload, or None when there is none or the
+    kernel sources changed since it was taken."""
+    path = os.path.join(PROFILES, f"k_vmm_dot2_traffic_{workload}_b{budget}.md")
+    if not os.path.exists(path):
+        return None
+    fields = {}
+    with open(path) as f:
+        for line in f:
+            if ":" in line and not line.startswith(("#", "|", " ")):
+                k, v = line.split(":", 1)
+                fields[k.strip()] = v.strip()
+    if fields.get("source_sha256_16") != vmm_source_sha():
+        return None
+    try:
+        return float(fields["traffic_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def copy_calibration(mib: int, reps: int):
+    """A plain device-to-device copy of known size, for scaling the HBM byte
+    counters (run under rocprofv3 --pmc)."""
+    import torch
+    n = mib << 20
+    src = torch.ones(n, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(reps):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes_read": n, "copy_bytes_written": n, "reps": reps}), flush=True)
+
+
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -57,6 +105,10 @@ def parse():
     ap.add_argument("--tile-n", type=int, default=0)
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
     ap.add_argument("--vmm-only-reps", type=int, default=5)
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="only run a plain copy of MIB MiB (counter calibration) and exit")
+    ap.add_argument("--vmm-source-sha", action="store_true",
+                    help="print the hash of the VMM kernel sources and exit")
     return ap.parse_args()
 
 
@@ -104,10 +156,17 @@ def cpu_baseline(wl, budget, tokens_sample: int):
 
 def main():
     args = parse()
+    if args.vmm_source_sha:
+        print(vmm_source_sha())
+        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the nested-precision "
               "VMM path has no multi-GPU mode in this build.", file=sys.stderr)
         sys.exit(2)
+
+    if args.copy_calibration:
+        copy_calibration(args.copy_calibration, reps=10)
+        return
 
     import torch
     from paper_2606_23419_amd import grinqh as g
@@ -273,7 +332,9 @@ def main():
         "us_per_vmm": round(us_per_vmm, 3),
         "per_layer": per_layer,
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None},
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                     "traffic": stored_traffic(args.workload, budget)},
+        "algorithmic_bytes_per_vmm": round(bytes_per_vmm, 1),
     }
     if not args.no_cpu:
         out["cpu_baseline"] = cpu_baseline(wl, budget, tokens_sample=8)
