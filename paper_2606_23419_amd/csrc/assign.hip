@@ -21,183 +21,218 @@ __global__ __launch_bounds__(256) void k_assign_threshold(const uint16_t* __rest
   lm[i] = (uint8_t)l;
 }
 
-// Top-k: one workgroup of 1024 threads per token, every key in registers
-// (K <= 16384).  For every level j the cut is the C_j-th largest key (C_j =
-// channels at level >= j).  A two-digit radix select finds all cuts at once:
-// per-wave LDS histograms of the high 8 bits, a parallel suffix scan to find
-// the bin holding each cut, then 128-bin histograms of the low 7 bits inside
-// those bins.  Channels strictly above the cut key are in.  Of the channels
-// equal to it, the first ones in index order are in: per-(chunk, wave) ballots
-// of key == cut are stored, and one wave per level walks them in index order
-// to find the channel index where the count reaches the number still needed.
-constexpr int kTopkThreads = 1024;
-constexpr int kTopkWaves = kTopkThreads / 64;
-constexpr int kTopkPer = 16;                     // keys per thread
-constexpr int kTopkMaxK = kTopkThreads * kTopkPer;
+// Top-k: one workgroup of 512 threads per token, K <= 16384, every key in
+// registers.  For every level j the cut is the C_j-th largest key (C_j =
+// channels at level >= j); channels strictly above it are in, and of those
+// equal to it the first ones in channel order.
+//   1. A histogram of all 2^15 key values (two 16-bit counts per LDS word) and
+//      per-thread totals of 64 consecutive values.
+//   2. Wave j finds cut j: a wave scan over the totals picks the thread range,
+//      a second one the key value; then it counts the channels equal to the cut
+//      key in channel order (each lane a contiguous span of the keys kept in
+//      LDS), picks the lane and the 8-key chunk where the count reaches the
+//      number still needed, and from it the channel-index limit.
+//   3. Every thread grades its channels against the cuts.
+constexpr int kTkThreads = 512;
+constexpr int kTkChunk = kTkThreads * 8;   // channels per load round, 8 per thread
+constexpr int kTkMaxK = 16384;
+constexpr int kTkBins = 1 << 15;           // every 15-bit key value
 constexpr int kCuts = kMaxLevels - 1;
 
-__device__ __forceinline__ uint32_t incl_scan64(uint32_t v, int lane) {
-#pragma unroll
-  for (int off = 1; off < 64; off <<= 1) {
-    const uint32_t o = __shfl_up(v, off);
-    if (lane >= off) v += o;
-  }
+// Inclusive prefix sum over the 64 lanes: shifts within rows of 16 lanes, then
+// the row broadcasts of lanes 15 and 31.
+__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t v) {
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x111, 0xF, 0xF, false);   // row_shr:1
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x112, 0xF, 0xF, false);   // row_shr:2
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x114, 0xF, 0xF, false);   // row_shr:4
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x118, 0xF, 0xF, false);   // row_shr:8
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x142, 0xA, 0xF, false);   // row_bcast:15
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x143, 0xC, 0xF, false);   // row_bcast:31
   return v;
 }
 
-// Position (0..63) of the r-th set bit (r >= 1) of m.
-__device__ __forceinline__ int nth_set_bit(uint64_t m, int r) {
-  int pos = 0;
-#pragma unroll
-  for (int w = 32; w > 0; w >>= 1) {
-    const uint64_t low = m & ((w == 64 ? ~0ull : (1ull << w) - 1ull));
-    const int c = __popcll(low);
-    if (r > c) {
-      r -= c;
-      m >>= w;
-      pos += w;
-    } else {
-      m = low;
-    }
-  }
-  return pos;
+typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ int first_lane(bool pred) {
+  const uint64_t m = __ballot(pred);
+  return m ? (int)__builtin_ctzll(m) : 0;
 }
 
-__global__ __launch_bounds__(kTopkThreads) void k_assign_topk(const uint16_t* __restrict__ x,
-                                                              uint8_t* __restrict__ lm, int K,
-                                                              TopkCuts cuts) {
-  __shared__ uint32_t s_h1[kTopkWaves][256];
-  __shared__ uint32_t s_h2[kCuts][128];
-  __shared__ uint32_t s_wsum[kTopkWaves];
-  __shared__ int s_cut_bin[kCuts], s_need[kCuts], s_need_eq[kCuts], s_idx_lim[kCuts];
-  __shared__ uint32_t s_cut_key[kCuts];
-  __shared__ uint64_t s_bal[kTopkPer][kTopkWaves][kCuts];
+__device__ __forceinline__ uint32_t readlane(uint32_t v, int l) {
+  return (uint32_t)__builtin_amdgcn_readlane((int)v, l);
+}
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+__device__ __forceinline__ int count_eq8(const uint4& w, uint32_t key) {
+  const uint32_t a[4] = {w.x, w.y, w.z, w.w};
+  int c = 0;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) c += ((a[i] & 0xFFFFu) == key) + ((a[i] >> 16) == key);
+  return c;
+}
+
+template <int R>
+__global__ __launch_bounds__(kTkThreads) void k_assign_topk(const uint16_t* __restrict__ x,
+                                                            uint8_t* __restrict__ lm, int K,
+                                                            TopkCuts cuts) {
+  __shared__ uint32_t s_hist[kTkBins / 2];
+  __shared__ __attribute__((aligned(16))) uint16_t s_key[kTkMaxK + 64 * 32];
+  __shared__ __attribute__((aligned(16))) uint32_t s_tot[kTkThreads];
+  __shared__ uint32_t s_cut[kCuts];
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int n = cuts.n;
-  const int M = (K + kTopkThreads - 1) / kTopkThreads;
   const uint16_t* xt = x + (size_t)blockIdx.x * K;
   uint8_t* out = lm + (size_t)blockIdx.x * K;
+  const int span = (K + 2047) / 2048 * 32;   // keys per lane in the tie scans; 64*span >= K
 
-  uint32_t key[kTopkPer];
+  // round r: channels r*kTkChunk + 8*tid .. +7 (K is a multiple of 128).  The
+  // address is clamped so that every thread loads; invalid rounds are unused.
+  uint32_t kw[R][4];
 #pragma unroll
-  for (int m = 0; m < kTopkPer; ++m) {
-    const int k = m * kTopkThreads + tid;
-    key[m] = (m < M && k < K) ? mag_key(xt[k]) : 0xFFFFu;   // 0xFFFF: no channel
-  }
-  for (int i = tid; i < kTopkWaves * 256; i += kTopkThreads) (&s_h1[0][0])[i] = 0u;
-  for (int i = tid; i < kCuts * 128; i += kTopkThreads) (&s_h2[0][0])[i] = 0u;
-  if (tid < kCuts) {
-    s_cut_bin[tid] = 256;
-    s_need[tid] = 0;
-    s_cut_key[tid] = 0x8000u;   // above every key: nobody is in
-    s_need_eq[tid] = 0;
-    s_idx_lim[tid] = 0;
-  }
-  __syncthreads();
-
-  // high-digit histograms, one per wave
+  for (int r = 0; r < R; ++r) {
+    const int k0 = min(r * kTkChunk + 8 * tid, K - 8);
+    uint32_t v[4];
+    __builtin_memcpy(v, xt + k0, 16);
 #pragma unroll
-  for (int m = 0; m < kTopkPer; ++m)
-    if (key[m] != 0xFFFFu) atomicAdd(&s_h1[wave][key[m] >> 7], 1u);
+    for (int i = 0; i < 4; ++i) kw[r][i] = v[i] & 0x7FFF7FFFu;
+  }
+  for (int i = tid; i < kTkBins / 8; i += kTkThreads) reinterpret_cast<uint4*>(s_hist)[i] = uint4{0u, 0u, 0u, 0u};
+  for (int i = K + tid; i < 64 * span; i += kTkThreads) s_key[i] = 0xFFFFu;
+#pragma unroll
+  for (int r = 0; r < R; ++r)
+    if (r * kTkChunk + 8 * tid < K)
+      *reinterpret_cast<uint4*>(&s_key[r * kTkChunk + 8 * tid]) = uint4{kw[r][0], kw[r][1], kw[r][2], kw[r][3]};
   __syncthreads();
 
-  // suffix counts over bins: thread i < 256 takes bin 255 - i
-  uint32_t tot = 0, incl = 0;
-  if (tid < 256) {
-    const int b = 255 - tid;
-    for (int w = 0; w < kTopkWaves; ++w) tot += s_h1[w][b];
-    incl = incl_scan64(tot, lane);
-    if (lane == 63) s_wsum[wave] = incl;
-  }
-  __syncthreads();
-  if (tid < 256) {
-    for (int w = 0; w < wave; ++w) incl += s_wsum[w];
-    const uint32_t above = incl - tot;   // keys in higher bins
-    for (int j = 0; j < n; ++j) {
-      const uint32_t C = (uint32_t)cuts.cum[j];
-      if (C > above && C <= incl) {
-        s_cut_bin[j] = 255 - tid;
-        s_need[j] = (int)(C - above);
-      }
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    if (r * kTkChunk + 8 * tid >= K) continue;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const uint32_t key = (kw[r][i >> 1] >> (16 * (i & 1))) & 0xFFFFu;
+      atomicAdd(&s_hist[key >> 1], 1u << (16 * (key & 1u)));
     }
   }
   __syncthreads();
 
-  // low-digit histograms inside each cut bin
+  {   // thread t: key values 64t .. 64t+63; 16-bit lanes cannot overflow (K < 2^16)
+    u16x2 acc = {0, 0};
 #pragma unroll
-  for (int m = 0; m < kTopkPer; ++m) {
-    if (key[m] == 0xFFFFu) continue;
-    const int hi = (int)(key[m] >> 7);
-    for (int j = 0; j < n; ++j)
-      if (hi == s_cut_bin[j]) atomicAdd(&s_h2[j][key[m] & 127u], 1u);
-  }
-  __syncthreads();
-
-  // per level j (threads 128 j .. 128 j + 127), suffix over sub-bins
-  {
-    const int j = tid >> 7, i = tid & 127, sb = 127 - i;
-    const uint32_t h = j < n ? s_h2[j][sb] : 0u;
-    uint32_t inc2 = incl_scan64(h, lane);
-    if (lane == 63) s_wsum[wave] = inc2;
-    __syncthreads();
-    if (wave & 1) inc2 += s_wsum[wave - 1];
-    if (j < n && s_cut_bin[j] < 256) {
-      const uint32_t need = (uint32_t)s_need[j];
-      const uint32_t above = inc2 - h;
-      if (need > above && need <= inc2) {
-        s_cut_key[j] = ((uint32_t)s_cut_bin[j] << 7) | (uint32_t)sb;
-        s_need_eq[j] = (int)(need - above);
-      }
+    for (int i = 0; i < 8; ++i) {
+      // rotated so that the lanes of a wave hit different LDS banks
+      const uint4 w = reinterpret_cast<const uint4*>(s_hist)[8 * tid + ((i + tid) & 7)];
+      acc += __builtin_bit_cast(u16x2, w.x) + __builtin_bit_cast(u16x2, w.y) +
+             __builtin_bit_cast(u16x2, w.z) + __builtin_bit_cast(u16x2, w.w);
     }
+    s_tot[tid] = (uint32_t)acc[0] + (uint32_t)acc[1];
   }
   __syncthreads();
 
-  // ballots of key == cut key, per (chunk, wave, level)
-#pragma unroll
-  for (int m = 0; m < kTopkPer; ++m) {
-    if (m >= M) break;
-    for (int j = 0; j < n; ++j) {
-      const uint64_t bal = __ballot(key[m] == s_cut_key[j]);
-      if (lane == 0) s_bal[m][wave][j] = bal;
-    }
-  }
-  __syncthreads();
-
-  // wave j finds the index of the need_eq-th channel equal to cut key j
   if (wave < n) {
     const int j = wave;
-    const int need = s_need_eq[j];
-    const int E = M * kTopkWaves;
-    int carry = 0;
-    for (int base = 0; base < E && need > 0; base += 64) {
-      const int e = base + lane;
-      const uint64_t bal = e < E ? s_bal[e / kTopkWaves][e % kTopkWaves][j] : 0ull;
-      const uint32_t c = (uint32_t)__popcll(bal);
-      const uint32_t inc = incl_scan64(c, lane) + (uint32_t)carry;
-      const uint32_t before = inc - c;
-      if ((uint32_t)need > before && (uint32_t)need <= inc) {
-        const int bit = nth_set_bit(bal, need - (int)before);
-        // entry e covers channels (e / 16) * 1024 + (e % 16) * 64 + bit
-        s_idx_lim[j] = (e / kTopkWaves) * kTopkThreads + (e % kTopkWaves) * 64 + bit + 1;
+    const uint32_t C = (uint32_t)cuts.cum[j];
+    uint32_t ck = 0x8000u;   // above every key: nobody is in
+    int lim = 0;
+    if (C > 0) {
+      // lane l: threads 8l .. 8l+7, i.e. key values 512 l .. 512 l + 511
+      const uint4 a = reinterpret_cast<const uint4*>(s_tot)[2 * lane];
+      const uint4 b = reinterpret_cast<const uint4*>(s_tot)[2 * lane + 1];
+      const uint32_t sl = a.x + a.y + a.z + a.w + b.x + b.y + b.z + b.w;
+      const uint32_t pre = wave_incl_scan(sl);
+      const uint32_t above_l = readlane(pre, 63) - pre;          // keys in higher lanes
+      // inside each lane, from its highest thread down: the thread whose range
+      // holds the C-th largest key, if this lane's range does
+      const uint32_t tv[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+      uint32_t acc = above_l, q_loc = 0, above_loc = 0;
+#pragma unroll
+      for (int i = 7; i >= 0; --i) {
+        if (acc < C && C <= acc + tv[i]) {
+          q_loc = (uint32_t)i;
+          above_loc = acc;
+        }
+        acc += tv[i];
       }
-      carry = (int)__shfl(inc, 63);
-      if (carry >= need) break;
+      const int L = first_lane(above_l < C && C <= above_l + sl);
+      const int t_own = 8 * L + (int)readlane(q_loc, L);
+      const uint32_t above2 = readlane(above_loc, L);
+      // the 64 key values of that thread
+      const int kv = 64 * t_own + lane;
+      const uint32_t c = (reinterpret_cast<const uint16_t*>(s_hist))[kv];
+      const uint32_t pre64 = wave_incl_scan(c);
+      const uint32_t above_v = above2 + readlane(pre64, 63) - pre64;
+      const int bsel = first_lane(above_v < C && C <= above_v + c);
+      ck = (uint32_t)(64 * t_own + bsel);
+      const int need = (int)(C - readlane(above_v, bsel));        // >= 1 channels equal to ck
+      if (need == (int)readlane(c, bsel)) {   // every channel equal to ck is in
+        lim = K;
+        goto store;
+      }
+      // channels equal to ck, in channel order: lane l scans keys [l*span, (l+1)*span)
+      const int nch = span / 8;     // a multiple of 4
+      int e = 0, c8 = lane % nch;   // chunks visited in rotated order (LDS banks)
+      for (int i = 0; i < nch; i += 4) {
+        uint4 w[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          w[q] = *reinterpret_cast<const uint4*>(&s_key[lane * span + 8 * c8]);
+          c8 = c8 + 1 == nch ? 0 : c8 + 1;
+        }
+#pragma unroll
+        for (int q = 0; q < 4; ++q) e += count_eq8(w[q], ck);
+      }
+      const int pre_e = (int)wave_incl_scan((uint32_t)e);
+      const int L2 = first_lane(pre_e - e < need && need <= pre_e);
+      const int r1 = need - (int)readlane((uint32_t)(pre_e - e), L2);
+      // the 8-key chunks of lane L2's span
+      const int ec = lane < nch ? count_eq8(*reinterpret_cast<const uint4*>(&s_key[L2 * span + 8 * lane]), ck) : 0;
+      const int pre_c = (int)wave_incl_scan((uint32_t)ec);
+      const int cs = first_lane(lane < nch && pre_c - ec < r1 && r1 <= pre_c);
+      int r2 = r1 - (int)readlane((uint32_t)(pre_c - ec), cs);
+      const int base = L2 * span + 8 * cs;
+      const uint4 w8 = *reinterpret_cast<const uint4*>(&s_key[base]);
+      const uint32_t ww[4] = {w8.x, w8.y, w8.z, w8.w};
+      int pos = 0, seen = 0;   // the r2-th key equal to ck in this chunk
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const bool eq = ((ww[i >> 1] >> (16 * (i & 1))) & 0xFFFFu) == ck;
+        seen += eq ? 1 : 0;
+        if (eq && seen == r2) pos = i;
+      }
+      lim = base + pos + 1;
     }
+  store:
+    // channel k is in iff key > ck, or key == ck and k < lim: with the
+    // composite key*2^16 + (65535 - k), iff composite >= ck*2^16 + 65536 - lim.
+    if (lane == 0) s_cut[j] = C > 0 ? (ck << 16) + 65536u - (uint32_t)lim : 0xFFFFFFFFu;
   }
   __syncthreads();
 
+  // level = number of cuts passed; count the cuts not passed
+  uint32_t comp[R][8], miss[R][8];
 #pragma unroll
-  for (int m = 0; m < kTopkPer; ++m) {
-    if (m >= M) break;
-    const int k = m * kTopkThreads + tid;
-    if (k >= K) continue;
-    int lvl = 0;
-    for (int j = 0; j < n; ++j) {
-      const uint32_t ck = s_cut_key[j];
-      lvl += (key[m] > ck || (key[m] == ck && k < s_idx_lim[j])) ? 1 : 0;
+  for (int r = 0; r < R; ++r)
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const uint32_t key = (kw[r][i >> 1] >> (16 * (i & 1))) & 0xFFFFu;
+      comp[r][i] = (key << 16) + (uint32_t)(65535 - (r * kTkChunk + 8 * tid + i));
+      miss[r][i] = 0;
     }
-    out[k] = (uint8_t)lvl;
+  for (int j = 0; j < n; ++j) {
+    const uint32_t cc = s_cut[j];
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+#pragma unroll
+      for (int i = 0; i < 8; ++i) miss[r][i] += comp[r][i] < cc ? 1u : 0u;
+  }
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    const int k0 = r * kTkChunk + 8 * tid;
+    if (k0 >= K) continue;
+    uint32_t lv[2] = {0u, 0u};
+#pragma unroll
+    for (int i = 0; i < 8; ++i) lv[i >> 2] |= ((uint32_t)n - miss[r][i]) << (8 * (i & 3));
+    __builtin_memcpy(out + k0, lv, 8);
   }
 }
 
@@ -211,8 +246,16 @@ int launch_assign_threshold(const Layer& L, const void* x, int B, const Threshol
 
 int launch_assign_topk(const Layer& L, const void* x, int B, const TopkCuts& cuts,
                        uint8_t* level_map, hipStream_t s) {
-  hipLaunchKernelGGL(k_assign_topk, dim3((unsigned)B), dim3(kTopkThreads), 0, s,
-                     (const uint16_t*)x, level_map, L.K, cuts);
+  if (L.K > kTkMaxK || L.K % 8 != 0) return fail(GRINQH_EUNSUPPORTED, "top-k needs K <= %d", kTkMaxK);
+  const int rounds = (L.K + kTkChunk - 1) / kTkChunk;
+  const dim3 grid((unsigned)B), block(kTkThreads);
+  const uint16_t* xx = (const uint16_t*)x;
+  switch (rounds) {
+    case 1: hipLaunchKernelGGL(k_assign_topk<1>, grid, block, 0, s, xx, level_map, L.K, cuts); break;
+    case 2: hipLaunchKernelGGL(k_assign_topk<2>, grid, block, 0, s, xx, level_map, L.K, cuts); break;
+    case 3: hipLaunchKernelGGL(k_assign_topk<3>, grid, block, 0, s, xx, level_map, L.K, cuts); break;
+    default: hipLaunchKernelGGL(k_assign_topk<4>, grid, block, 0, s, xx, level_map, L.K, cuts); break;
+  }
   return check_launch("assign (top-k)");
 }
 
