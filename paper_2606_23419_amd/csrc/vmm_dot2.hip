@@ -52,19 +52,6 @@ __device__ __forceinline__ int lanes_below(bool pred) {
 }
 __device__ __forceinline__ int lanes_total(bool pred) { return (int)__popcll(__ballot(pred)); }
 
-// Make this wave's LDS writes visible to its own later LDS reads.
-__device__ __forceinline__ void wave_lds_sync() {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-  __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-}
-
-__device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
-  return v;
-}
-
 // Per-pair descriptor: byte offsets of the two plane chunks from the tile
 // base, the fp16x2 exponent bits for field position 4, and one fp16x2
 // coefficient pair per token (0 where that token does not read the plane).
