@@ -287,18 +287,35 @@ def unpack_prefix(packed: np.ndarray, N: int, K: int, plane_bits: int, tile_n: i
 
 
 def calibrate_thresholds(samples_abs, p_bp) -> np.ndarray:
-    """Offline threshold calibration (Sec. 3.2; App. A.1).
+    """Offline threshold calibration (Sec. 3.2; App. A.1; reading R16).
 
     For every calibration sample the thresholds are the magnitudes that split
-    |x| into the fractions P: theta_k is the (sum_{j<k} p_j)-th percentile of
-    that sample's magnitudes (numpy 'linear' interpolation); the per-sample
-    thresholds are then averaged.  Returns theta_1..theta_n (fp32).
+    |x| into the fractions P: theta_k is the sample quantile (type 7 of
+    Hyndman and Fan) of that sample's magnitudes at q_k = U_k / 10000,
+    U_k = sum_{j<k} p_j in basis points.  With the n magnitudes sorted
+    ascending (a_0 <= ... <= a_(n-1)), the position h = (n-1) U_k / 10000 is
+    taken exactly: lo = floor(h), frac = the fraction of h as a float64
+    quotient of integers, and theta = a_lo + frac * (a_(lo+1) - a_lo) in
+    float64 (a_(lo+1) = a_lo when lo = n-1).  The per-sample thresholds are
+    then averaged in float64, summed in sample order, and rounded to fp32.
+    Returns theta_1..theta_n.
     """
-    p = np.asarray(p_bp, dtype=np.float64) / 10000.0
-    n = len(p) - 1
-    per_sample = []
+    p = [int(v) for v in p_bp]
+    n_th = len(p) - 1
+    acc = np.zeros(n_th, dtype=np.float64)
+    count = 0
     for a in samples_abs:
-        a = np.asarray(a, dtype=np.float64).reshape(-1)
-        ths = [np.percentile(a, 100.0 * float(np.sum(p[:k]))) for k in range(1, n + 1)]
-        per_sample.append(ths)
-    return np.mean(np.asarray(per_sample), axis=0).astype(np.float32)
+        srt = np.sort(np.asarray(a, dtype=np.float64).reshape(-1))
+        n = srt.size
+        ths = np.empty(n_th, dtype=np.float64)
+        for k in range(1, n_th + 1):
+            U = sum(p[:k])
+            num = (n - 1) * U                      # h = num / 10000, exactly
+            lo = num // 10000
+            frac = np.float64(num % 10000) / np.float64(10000.0)
+            lo_v = srt[lo]
+            hi_v = srt[min(lo + 1, n - 1)]
+            ths[k - 1] = lo_v + frac * (hi_v - lo_v)
+        acc = acc + ths
+        count += 1
+    return (acc / np.float64(count)).astype(np.float32)

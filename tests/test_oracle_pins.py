@@ -258,6 +258,30 @@ def test_topk_exact_budget_on_workload_shapes():
             assert np.all(np.diff(lv[t][order].astype(int)) <= 0)
 
 
+def test_calibration_matches_library_quantiles():
+    # type-7 sample quantiles are numpy's 'linear' percentiles; the oracle
+    # fixes the position exactly, so the two agree to rounding
+    rng = np.random.default_rng(93)
+    for n in (128, 1000, 4096):
+        samples = [np.abs(rng.standard_t(3, n)).astype(np.float16).astype(np.float64) for _ in range(5)]
+        for p in [(2000, 800, 2400, 4800, 0), (0, 0, 0, 10000), (2500, 2500, 2500, 2500), (3333, 3333, 3334)]:
+            cum = np.cumsum(p)[:-1]
+            lib = np.mean([[np.percentile(a, c / 100.0) for c in cum] for a in samples], axis=0)
+            ours = orc.calibrate_thresholds(samples, p)
+            np.testing.assert_allclose(ours, lib.astype(np.float32), rtol=2e-7, atol=0)
+
+
+def test_calibration_exact_small_case():
+    # n = 5 magnitudes 1..5, quantiles at 25% and 60%: h = 1.0 and 2.4
+    a = np.array([5.0, 1.0, 4.0, 2.0, 3.0])
+    th = orc.calibrate_thresholds([a], (2500, 3500, 4000))
+    assert th[0] == np.float32(2.0)
+    assert th[1] == np.float32(3.0 + 0.4 * 1.0)
+    # two samples: the mean of the per-sample values
+    th2 = orc.calibrate_thresholds([a, 2 * a], (2500, 7500))
+    assert th2[0] == np.float32((2.0 + 4.0) / 2)
+
+
 def test_calibrated_thresholds_reproduce_fractions_on_one_sample():
     a = np.abs(inputs.activations_t3(4096, 1, config=92)[0].astype(np.float64))
     p = (2000, 2000, 3000, 3000)
