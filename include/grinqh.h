@@ -113,6 +113,23 @@ GRINQH_API int grinqh_topk_counts(int32_t K, int32_t n_levels, const int32_t* p_
  * present kernels need none and report 0; callers may pass NULL/0. */
 GRINQH_API int grinqh_workspace_bytes(const grinqh_layer_desc* desc, int32_t B, size_t* bytes);
 
+/* Offline threshold calibration (Sec. 3.2 calibration of the thresholds;
+ * App. A.1).  x: fp16 [S][K] (device) calibration activations, one sample per
+ * row, finite; p_bp: host int32 p_0..p_n in basis points (each >= 0, summing
+ * to 10000).  For each sample and each k = 1..n (n = n_levels-1) the sample
+ * threshold is the type-7 sample quantile of |x| at q_k = U_k / 10000, U_k =
+ * p_0 + .. + p_(k-1): with the K magnitudes sorted ascending a_0 <= .. <=
+ * a_(K-1), h = (K-1) U_k / 10000 is split exactly into lo = floor(h) and
+ * frac = (h - lo) as a float64 quotient of integers, and the threshold is
+ * a_lo + frac * (a_(lo+1) - a_lo) in float64 (a_(lo+1) = a_lo at lo = K-1).
+ * theta_k is the float64 mean of the sample thresholds, summed in sample
+ * order, rounded to fp32.
+ *   per_sample: device float64 [S][n] scratch, written (8-byte aligned).
+ *   theta: device fp32 [n] out.  Requires 1 <= S <= 65535, K <= 16384. */
+GRINQH_API int grinqh_calibrate(const grinqh_layer_desc* desc, const void* x, int32_t S,
+                                const int32_t* p_bp, double* per_sample, float* theta,
+                                void* stream);
+
 /* Per-token precision assignment (Sec. 3.1; App. A.1).
  *   x: fp16 [B][K] (device), finite.
  *   mode GRINQH_ASSIGN_THRESHOLD: thresholds = host fp32 theta_1..theta_n

@@ -70,6 +70,88 @@ __device__ __forceinline__ int count_eq8(const uint4& w, uint32_t key) {
   return c;
 }
 
+// Round r of thread tid holds channels r*kTkChunk + 8*tid .. +7 as eight
+// 15-bit |x| keys packed in pairs (K is a multiple of 128).  The address is
+// clamped so that every thread loads; rounds past K are not used.
+template <int R>
+__device__ __forceinline__ void load_keys(const uint16_t* xt, int K, int tid, uint32_t (&kw)[R][4]) {
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    const int k0 = min(r * kTkChunk + 8 * tid, K - 8);
+    uint32_t v[4];
+    __builtin_memcpy(v, xt + k0, 16);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) kw[r][i] = v[i] & 0x7FFF7FFFu;
+  }
+}
+
+// Histogram of every key value, two 16-bit counts per word (s_hist zeroed and
+// a barrier passed before), then per-thread totals of 64 consecutive values:
+// thread t covers key values 64t .. 64t+63.  Ends with a barrier.
+template <int R>
+__device__ __forceinline__ void key_histogram(const uint32_t (&kw)[R][4], int K, int tid,
+                                              uint32_t* s_hist, uint32_t* s_tot) {
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    if (r * kTkChunk + 8 * tid >= K) continue;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const uint32_t key = (kw[r][i >> 1] >> (16 * (i & 1))) & 0xFFFFu;
+      atomicAdd(&s_hist[key >> 1], 1u << (16 * (key & 1u)));
+    }
+  }
+  __syncthreads();
+  {   // 16-bit lanes cannot overflow (K < 2^16)
+    u16x2 acc = {0, 0};
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      // rotated so that the lanes of a wave hit different LDS banks
+      const uint4 w = reinterpret_cast<const uint4*>(s_hist)[8 * tid + ((i + tid) & 7)];
+      acc += __builtin_bit_cast(u16x2, w.x) + __builtin_bit_cast(u16x2, w.y) +
+             __builtin_bit_cast(u16x2, w.z) + __builtin_bit_cast(u16x2, w.w);
+    }
+    s_tot[tid] = (uint32_t)acc[0] + (uint32_t)acc[1];
+  }
+  __syncthreads();
+}
+
+// One wave: the C-th largest key (1 <= C <= number of keys), found from the
+// per-thread totals and then the owning thread's 64 counts.  Returns the key;
+// *above = keys strictly greater, *equal = keys equal to it.
+__device__ __forceinline__ uint32_t select_key(uint32_t C, const uint32_t* s_hist,
+                                               const uint32_t* s_tot, int lane, uint32_t* above,
+                                               uint32_t* equal) {
+  // lane l: threads 8l .. 8l+7, i.e. key values 512 l .. 512 l + 511
+  const uint4 a = reinterpret_cast<const uint4*>(s_tot)[2 * lane];
+  const uint4 b = reinterpret_cast<const uint4*>(s_tot)[2 * lane + 1];
+  const uint32_t sl = a.x + a.y + a.z + a.w + b.x + b.y + b.z + b.w;
+  const uint32_t pre = wave_incl_scan(sl);
+  const uint32_t above_l = readlane(pre, 63) - pre;          // keys in higher lanes
+  // inside each lane, from its highest thread down: the thread whose range
+  // holds the C-th largest key, if this lane's range does
+  const uint32_t tv[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+  uint32_t acc = above_l, q_loc = 0, above_loc = 0;
+#pragma unroll
+  for (int i = 7; i >= 0; --i) {
+    if (acc < C && C <= acc + tv[i]) {
+      q_loc = (uint32_t)i;
+      above_loc = acc;
+    }
+    acc += tv[i];
+  }
+  const int L = first_lane(above_l < C && C <= above_l + sl);
+  const int t_own = 8 * L + (int)readlane(q_loc, L);
+  const uint32_t above2 = readlane(above_loc, L);
+  // the 64 key values of that thread
+  const uint32_t c = (reinterpret_cast<const uint16_t*>(s_hist))[64 * t_own + lane];
+  const uint32_t pre64 = wave_incl_scan(c);
+  const uint32_t above_v = above2 + readlane(pre64, 63) - pre64;
+  const int bsel = first_lane(above_v < C && C <= above_v + c);
+  *above = readlane(above_v, bsel);
+  *equal = readlane(c, bsel);
+  return (uint32_t)(64 * t_own + bsel);
+}
+
 template <int R>
 __global__ __launch_bounds__(kTkThreads) void k_assign_topk(const uint16_t* __restrict__ x,
                                                             uint8_t* __restrict__ lm, int K,
@@ -86,17 +168,8 @@ __global__ __launch_bounds__(kTkThreads) void k_assign_topk(const uint16_t* __re
   uint8_t* out = lm + (size_t)blockIdx.x * K;
   const int span = (K + 2047) / 2048 * 32;   // keys per lane in the tie scans; 64*span >= K
 
-  // round r: channels r*kTkChunk + 8*tid .. +7 (K is a multiple of 128).  The
-  // address is clamped so that every thread loads; invalid rounds are unused.
   uint32_t kw[R][4];
-#pragma unroll
-  for (int r = 0; r < R; ++r) {
-    const int k0 = min(r * kTkChunk + 8 * tid, K - 8);
-    uint32_t v[4];
-    __builtin_memcpy(v, xt + k0, 16);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) kw[r][i] = v[i] & 0x7FFF7FFFu;
-  }
+  load_keys<R>(xt, K, tid, kw);
   for (int i = tid; i < kTkBins / 8; i += kTkThreads) reinterpret_cast<uint4*>(s_hist)[i] = uint4{0u, 0u, 0u, 0u};
   for (int i = K + tid; i < 64 * span; i += kTkThreads) s_key[i] = 0xFFFFu;
 #pragma unroll
@@ -104,30 +177,7 @@ __global__ __launch_bounds__(kTkThreads) void k_assign_topk(const uint16_t* __re
     if (r * kTkChunk + 8 * tid < K)
       *reinterpret_cast<uint4*>(&s_key[r * kTkChunk + 8 * tid]) = uint4{kw[r][0], kw[r][1], kw[r][2], kw[r][3]};
   __syncthreads();
-
-#pragma unroll
-  for (int r = 0; r < R; ++r) {
-    if (r * kTkChunk + 8 * tid >= K) continue;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const uint32_t key = (kw[r][i >> 1] >> (16 * (i & 1))) & 0xFFFFu;
-      atomicAdd(&s_hist[key >> 1], 1u << (16 * (key & 1u)));
-    }
-  }
-  __syncthreads();
-
-  {   // thread t: key values 64t .. 64t+63; 16-bit lanes cannot overflow (K < 2^16)
-    u16x2 acc = {0, 0};
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      // rotated so that the lanes of a wave hit different LDS banks
-      const uint4 w = reinterpret_cast<const uint4*>(s_hist)[8 * tid + ((i + tid) & 7)];
-      acc += __builtin_bit_cast(u16x2, w.x) + __builtin_bit_cast(u16x2, w.y) +
-             __builtin_bit_cast(u16x2, w.z) + __builtin_bit_cast(u16x2, w.w);
-    }
-    s_tot[tid] = (uint32_t)acc[0] + (uint32_t)acc[1];
-  }
-  __syncthreads();
+  key_histogram<R>(kw, K, tid, s_hist, s_tot);
 
   if (wave < n) {
     const int j = wave;
@@ -135,36 +185,10 @@ __global__ __launch_bounds__(kTkThreads) void k_assign_topk(const uint16_t* __re
     uint32_t ck = 0x8000u;   // above every key: nobody is in
     int lim = 0;
     if (C > 0) {
-      // lane l: threads 8l .. 8l+7, i.e. key values 512 l .. 512 l + 511
-      const uint4 a = reinterpret_cast<const uint4*>(s_tot)[2 * lane];
-      const uint4 b = reinterpret_cast<const uint4*>(s_tot)[2 * lane + 1];
-      const uint32_t sl = a.x + a.y + a.z + a.w + b.x + b.y + b.z + b.w;
-      const uint32_t pre = wave_incl_scan(sl);
-      const uint32_t above_l = readlane(pre, 63) - pre;          // keys in higher lanes
-      // inside each lane, from its highest thread down: the thread whose range
-      // holds the C-th largest key, if this lane's range does
-      const uint32_t tv[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
-      uint32_t acc = above_l, q_loc = 0, above_loc = 0;
-#pragma unroll
-      for (int i = 7; i >= 0; --i) {
-        if (acc < C && C <= acc + tv[i]) {
-          q_loc = (uint32_t)i;
-          above_loc = acc;
-        }
-        acc += tv[i];
-      }
-      const int L = first_lane(above_l < C && C <= above_l + sl);
-      const int t_own = 8 * L + (int)readlane(q_loc, L);
-      const uint32_t above2 = readlane(above_loc, L);
-      // the 64 key values of that thread
-      const int kv = 64 * t_own + lane;
-      const uint32_t c = (reinterpret_cast<const uint16_t*>(s_hist))[kv];
-      const uint32_t pre64 = wave_incl_scan(c);
-      const uint32_t above_v = above2 + readlane(pre64, 63) - pre64;
-      const int bsel = first_lane(above_v < C && C <= above_v + c);
-      ck = (uint32_t)(64 * t_own + bsel);
-      const int need = (int)(C - readlane(above_v, bsel));        // >= 1 channels equal to ck
-      if (need == (int)readlane(c, bsel)) {   // every channel equal to ck is in
+      uint32_t above, equal;
+      ck = select_key(C, s_hist, s_tot, lane, &above, &equal);
+      const int need = (int)(C - above);        // >= 1 channels equal to ck
+      if (need == (int)equal) {   // every channel equal to ck is in
         lim = K;
         goto store;
       }
@@ -234,6 +258,68 @@ __global__ __launch_bounds__(kTkThreads) void k_assign_topk(const uint16_t* __re
     for (int i = 0; i < 8; ++i) lv[i >> 2] |= ((uint32_t)n - miss[r][i]) << (8 * (i & 3));
     __builtin_memcpy(out + k0, lv, 8);
   }
+}
+
+// Offline threshold calibration (Sec. 3.2; App. A.1).  One workgroup per
+// calibration sample: the two order statistics around each quantile position
+// come from the same key histogram as the top-k assignment, and lane 0 of
+// wave k interpolates threshold k in float64 (no contraction, so the
+// rounding is the plain one of each operation).
+template <int R>
+__global__ __launch_bounds__(kTkThreads) void k_calibrate_sample(const uint16_t* __restrict__ x,
+                                                                 int K, QuantilePos qp,
+                                                                 double* __restrict__ per_sample) {
+#pragma clang fp contract(off)
+  __shared__ uint32_t s_hist[kTkBins / 2];
+  __shared__ __attribute__((aligned(16))) uint32_t s_tot[kTkThreads];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const uint16_t* xt = x + (size_t)blockIdx.x * K;
+  uint32_t kw[R][4];
+  load_keys<R>(xt, K, tid, kw);
+  for (int i = tid; i < kTkBins / 8; i += kTkThreads) reinterpret_cast<uint4*>(s_hist)[i] = uint4{0u, 0u, 0u, 0u};
+  __syncthreads();
+  key_histogram<R>(kw, K, tid, s_hist, s_tot);
+  if (wave < qp.n) {
+    uint32_t above, equal;
+    // ascending rank r is the (K - r)-th largest
+    const uint32_t klo = select_key((uint32_t)(K - qp.lo[wave]), s_hist, s_tot, lane, &above, &equal);
+    const uint32_t khi = select_key((uint32_t)(K - qp.hi[wave]), s_hist, s_tot, lane, &above, &equal);
+    if (lane == 0) {
+      const double a = (double)h2f((uint16_t)klo), b = (double)h2f((uint16_t)khi);
+      const double d = b - a;
+      const double t = qp.frac[wave] * d;
+      per_sample[(size_t)blockIdx.x * qp.n + wave] = a + t;
+    }
+  }
+}
+
+__global__ void k_calibrate_mean(const double* __restrict__ per_sample, int S, int n,
+                                 float* __restrict__ theta) {
+#pragma clang fp contract(off)
+  const int k = threadIdx.x;
+  if (k >= n) return;
+  double acc = 0.0;
+  for (int s = 0; s < S; ++s) acc += per_sample[(size_t)s * n + k];
+  theta[k] = (float)(acc / (double)S);
+}
+
+int launch_calibrate(const Layer& L, const void* x, int S, const QuantilePos& qp,
+                     double* per_sample, float* theta, hipStream_t s) {
+  if (L.K > kTkMaxK || L.K % 8 != 0) return fail(GRINQH_EUNSUPPORTED, "calibration needs K <= %d", kTkMaxK);
+  const int rounds = (L.K + kTkChunk - 1) / kTkChunk;
+  const dim3 grid((unsigned)S), block(kTkThreads);
+  const uint16_t* xx = (const uint16_t*)x;
+  switch (rounds) {
+    case 1: hipLaunchKernelGGL(k_calibrate_sample<1>, grid, block, 0, s, xx, L.K, qp, per_sample); break;
+    case 2: hipLaunchKernelGGL(k_calibrate_sample<2>, grid, block, 0, s, xx, L.K, qp, per_sample); break;
+    case 3: hipLaunchKernelGGL(k_calibrate_sample<3>, grid, block, 0, s, xx, L.K, qp, per_sample); break;
+    default: hipLaunchKernelGGL(k_calibrate_sample<4>, grid, block, 0, s, xx, L.K, qp, per_sample); break;
+  }
+  int st = check_launch("calibrate (samples)");
+  if (st) return st;
+  hipLaunchKernelGGL(k_calibrate_mean, dim3(1), dim3(64), 0, s, per_sample, S, qp.n, theta);
+  return check_launch("calibrate (mean)");
 }
 
 int launch_assign_threshold(const Layer& L, const void* x, int B, const Thresholds& th,

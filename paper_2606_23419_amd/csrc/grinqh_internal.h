@@ -38,6 +38,14 @@ struct Thresholds {
   int n;
 };
 
+// Quantile positions for threshold calibration: ascending ranks lo/hi and
+// the interpolation fraction, per threshold.
+struct QuantilePos {
+  int lo[kMaxLevels - 1], hi[kMaxLevels - 1];
+  double frac[kMaxLevels - 1];
+  int n;
+};
+
 struct TopkCuts {
   int cum[kMaxLevels];           // cum[j] = C_{j+1}: channels at level >= j+1
   int n;
@@ -62,6 +70,12 @@ int launch_assign_threshold(const Layer& L, const void* x, int B, const Threshol
                             uint8_t* level_map, hipStream_t s);
 int launch_assign_topk(const Layer& L, const void* x, int B, const TopkCuts& cuts,
                        uint8_t* level_map, hipStream_t s);
+int launch_calibrate(const Layer& L, const void* x, int S, const QuantilePos& qp,
+                     double* per_sample, float* theta, hipStream_t s);
+bool vmm_pp_supported(const Layer& L, int B);
+int launch_vmm_pp(const Layer& L, const void* codes, const void* scales, const void* x,
+                  const uint8_t* level_map, const Thresholds* th, uint8_t* level_map_out,
+                  float* y, hipStream_t s);
 bool vmm_dot2_supported(const Layer& L);
 int launch_vmm_dot2(const Layer& L, const void* codes, const void* scales, const void* x,
                     const uint8_t* level_map, const Thresholds* th, uint8_t* level_map_out,

@@ -11,6 +11,8 @@
 //   beta_g = sum_{k in g, level > 0} x_k (phi_b - 128),
 // which is sum_k x_k * s * (t + phi - 128) with the scale factored out.
 // Lane groups are reduced through LDS and added into y with atomics.
+#include <cstdlib>
+
 #include "grinqh_internal.h"
 
 namespace grinqh {
@@ -111,7 +113,11 @@ int launch_vmm(const Layer& L, const void* codes, const void* scales, const void
     int st = check_launch("vmm zero-fill");
     if (st) return st;
   }
-  if (vmm_dot2_supported(L) && !(L.T == 1024 && B > 2))
+  const char* force = getenv("GRINQH_VMM_KERNEL");   // "dot2" or "v0": testing and timing only
+  const bool want_dot2 = force && force[0] == 'd', want_v0 = force && force[0] == 'v';
+  if (!want_dot2 && !want_v0 && vmm_pp_supported(L, B))
+    return launch_vmm_pp(L, codes, scales, x, level_map, th, level_map_out, y, s);
+  if (!want_v0 && vmm_dot2_supported(L) && !(L.T == 1024 && B > 2))
     return launch_vmm_dot2(L, codes, scales, x, level_map, th, level_map_out, B, y, s);
   // about 512 workgroups per token over the whole chip
   int ksplit = (512 + L.tiles - 1) / L.tiles;

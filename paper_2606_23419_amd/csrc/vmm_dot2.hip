@@ -28,29 +28,18 @@
 #include <cstdlib>
 
 #include "grinqh_internal.h"
+#include "vmm_common.h"
 
 namespace grinqh {
 
 namespace {
 
+using namespace vmmdev;
+
 constexpr int kMaxGW = 4;                    // groups per workgroup (B = 1)
 constexpr int max_gw(int nb) { return nb == 1 ? kMaxGW : 2; }   // LDS of the pair lists
 constexpr int kMaxItems = kGroup * 4;        // 128 rows x 4 planes
 constexpr int kMaxPairs = kMaxItems / 2;
-
-typedef _Float16 half2_t __attribute__((ext_vector_type(2)));
-
-__device__ __forceinline__ float dot2(uint32_t a, uint32_t b, float c) {
-  return __builtin_amdgcn_fdot2(__builtin_bit_cast(half2_t, a), __builtin_bit_cast(half2_t, b), c,
-                                false);
-}
-
-// Number of set predicates in lanes below this one, and in the whole wave.
-__device__ __forceinline__ int lanes_below(bool pred) {
-  const uint64_t m = __ballot(pred);
-  return (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
-}
-__device__ __forceinline__ int lanes_total(bool pred) { return (int)__popcll(__ballot(pred)); }
 
 // Per-pair descriptor: byte offsets of the two plane chunks from the tile
 // base, the fp16x2 exponent bits for field position 4, and one fp16x2
@@ -59,112 +48,6 @@ template <int NB>
 struct Desc {
   static constexpr int DW = NB == 1 ? 4 : 8;
 };
-
-// Sixteen outputs of one pair: w1/w2 are the two plane rows' dwords.
-template <int NB, int NACC>
-__device__ __forceinline__ void consume_pair(uint32_t w1, uint32_t w2, uint32_t m4,
-                                             const uint32_t (&xp)[NB], float (&acc)[NB][NACC],
-                                             int base) {
-  const uint32_t m6 = m4 - 0x08000800u;   // exponent field - 2 in both halves
-  const uint32_t m8 = m4 - 0x10001000u;   // exponent field - 4
-#pragma unroll
-  for (int h = 0; h < 2; ++h) {
-    const uint32_t R = __builtin_amdgcn_perm(w2, w1, h ? 0x07060302u : 0x05040100u);
-    const uint32_t A = R, Bv = R << 4, C = R >> 6;
-    uint32_t f[8];
-    f[0] = (Bv & 0x00300030u) | m4;   // field 0: bits 0-1 moved to 4-5
-    f[1] = (Bv & 0x00C000C0u) | m6;   // field 1: bits 2-3 -> 6-7
-    f[2] = (A & 0x00300030u) | m4;    // field 2: bits 4-5
-    f[3] = (A & 0x00C000C0u) | m6;    // field 3: bits 6-7
-    f[4] = (A & 0x03000300u) | m8;    // field 4: bits 8-9
-    f[5] = (C & 0x00300030u) | m4;    // field 5: bits 10-11 -> 4-5
-    f[6] = (C & 0x00C000C0u) | m6;    // field 6: bits 12-13 -> 6-7
-    f[7] = (C & 0x03000300u) | m8;    // field 7: bits 14-15 -> 8-9
-#pragma unroll
-    for (int e = 0; e < 8; ++e)
-#pragma unroll
-      for (int b = 0; b < NB; ++b) acc[b][base + h * 8 + e] = dot2(f[e], xp[b], acc[b][base + h * 8 + e]);
-  }
-}
-
-// 2^(4-p) for the field position p used by output e (mod 8) above: the
-// output's offset relative to the position-4 offset summed per pair.
-__device__ __forceinline__ float offset_factor(int e) {
-  const int m = e & 7;
-  return (m == 4 || m == 7) ? 0.0625f : ((m == 1 || m == 3 || m == 6) ? 0.25f : 1.0f);
-}
-
-__device__ __forceinline__ float phi_minus_offset(int b) {
-  return (b < 8 ? (float)(1 << (7 - b)) : 0.0f) - 128.0f;
-}
-
-template <int V>
-struct Words {
-  uint32_t w[V];
-};
-
-template <int V>
-__device__ __forceinline__ Words<V> load_words(const uint8_t* p) {
-  Words<V> r;
-  if constexpr (V == 1) {
-    r.w[0] = __builtin_nontemporal_load((const uint32_t*)p);
-  } else {
-    typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-    const u32x2 v = __builtin_nontemporal_load((const u32x2*)p);
-    r.w[0] = v.x;
-    r.w[1] = v.y;
-  }
-  return r;
-}
-
-// Sum of a value over the four 16-lane rows of a wave, in every lane.
-// v_permlane32_swap exchanges the upper 32 lanes of its first operand with
-// the lower 32 of its second, and v_permlane16_swap the odd rows of the first
-// with the even rows of the second; both write both registers.  They are
-// written as asm with both registers as in/out operands: the compiler's
-// builtins for them, given one value twice, have been seen to read back the
-// first result in place of the second.  s_nop 1 covers the VALU-write to
-// permlane-read hazard of the copy just before.
-__device__ __forceinline__ float row_sum4(float v) {
-  uint32_t a = __builtin_bit_cast(uint32_t, v), b = a;
-  asm volatile("s_nop 1\n\tv_permlane32_swap_b32 %0, %1" : "+v"(a), "+v"(b));
-  v = __builtin_bit_cast(float, a) + __builtin_bit_cast(float, b);   // rows r and r^2
-  a = __builtin_bit_cast(uint32_t, v);
-  b = a;
-  asm volatile("s_nop 1\n\tv_permlane16_swap_b32 %0, %1" : "+v"(a), "+v"(b));
-  return __builtin_bit_cast(float, a) + __builtin_bit_cast(float, b);  // and r^1
-}
-
-// Rotate right by n lanes inside each 16-lane row (DPP row_ror).
-template <int n>
-__device__ __forceinline__ float row_ror(float v) {
-  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v),
-                                                               0x120 + n, 0xF, 0xF, false));
-}
-
-// Sum over the whole wave, in every lane: row sums by rotation, then rows.
-__device__ __forceinline__ float wave_sum_dpp(float v) {
-  v += row_ror<8>(v);
-  v += row_ror<4>(v);
-  v += row_ror<2>(v);
-  v += row_ror<1>(v);
-  return row_sum4(v);
-}
-
-// Sum over the lane groups of a wave that hold the same outputs: LPR lanes
-// cover a plane row, so 64 / LPR lane groups share each output.
-template <int LPR>
-__device__ __forceinline__ float lane_group_sum(float v) {
-  if constexpr (LPR == 16) {
-    return row_sum4(v);
-  } else if constexpr (LPR == 32) {
-    uint32_t a = __builtin_bit_cast(uint32_t, v), b = a;
-    asm volatile("s_nop 1\n\tv_permlane32_swap_b32 %0, %1" : "+v"(a), "+v"(b));
-    return __builtin_bit_cast(float, a) + __builtin_bit_cast(float, b);
-  } else {
-    return v;
-  }
-}
 
 template <int V, int LPR, int NB, int PB, int kThreads>
 __global__ __launch_bounds__(kThreads) void k_vmm_dot2(

@@ -1,0 +1,383 @@
+// Nested-precision decode VMM at batch 1 for 2-bit planes, with a channel's
+// consecutive planes merged before the multiply-add (Sec. 3.3 reconstruction
+// with the midpoint bias; App. C.1 sparse bit-loading), laid out for CDNA4.
+//
+// A channel read to depth d planes contributes x_k * sum_j c_j 2^(8-2j).  Its
+// planes are taken as items: "doubles" for the plane pairs (1,2) and (3,4)
+// inside the depth, and a "single" for an odd last plane (depth 1 or 3).  A
+// double's two fields merge into one 4-bit field F = 4 c_j + c_(j+1) worth
+// F 2^(6-2j), so one fp16 operand carries four bits of the code instead of
+// two: for 16 outputs a lane turns its two plane dwords into two dwords of
+// 4-bit fields (even and odd outputs; a shift and a bit-field insert each),
+// and a v_and_or_b32 with the exponent bits E = 31 - 2j - p (fp16 bias 15)
+// makes the field at bit p of a half read as 2^(16-2j-p) + F 2^(6-2j).
+// v_perm_b32 puts one byte of each of two channels (two fields per byte) in
+// the two halves, so one v_dot2_f32_f16 with (x_k1, x_k2) adds both channels.
+// Singles are consumed as 2-bit fields exactly as in the general 2-bit kernel.
+//
+// Work units hold four plane dwords per lane: either two doubles (two
+// channels, planes j and j+1 each) or two pairs of singles.  A group's units
+// are listed doubles first, each kind padded to whole batches, so every batch
+// is of one kind and every unit issues the same four loads.  The offsets the
+// exponent bits add are summed per lane group, one sum per kind, and taken
+// out at the end of the group:
+//   y_n += s_{g,n} (acc_n - f_d(n) off_d - f_s(n) off_s + beta_g),
+// with f_d = 2^(-p) for doubles, f_s = 2^(4-p) for singles (p = the output's
+// field position) and beta_g = sum_{k: level > 0} x_k (phi_b - 128).
+#include <cstdlib>
+
+#include "grinqh_internal.h"
+#include "vmm_common.h"
+
+namespace grinqh {
+
+namespace {
+
+using namespace vmmdev;
+
+#ifndef GRINQH_PP_DEPTH
+#define GRINQH_PP_DEPTH 4
+#endif
+
+constexpr int kPPMaxGW = 4;        // groups per workgroup
+constexpr int kPPMaxUnits = 160;   // per group: <= 128 double units + 32 single units, padded
+
+// 16 outputs, two channels, planes (j, j+1) of each: w?a = plane j, w?b = j+1.
+__device__ __forceinline__ void consume_double(uint32_t w1a, uint32_t w1b, uint32_t w2a,
+                                               uint32_t w2b, uint32_t m0, uint32_t xp,
+                                               float (&acc)[16]) {
+  // 4-bit fields of the even outputs (E) and of the odd outputs (O), output
+  // 2m (or 2m+1) at bits 4m..4m+3 with the plane-j field on top
+  const uint32_t E1 = ((w1a << 2) & 0xCCCCCCCCu) | (w1b & 0x33333333u);
+  const uint32_t O1 = (w1a & 0xCCCCCCCCu) | ((w1b >> 2) & 0x33333333u);
+  const uint32_t E2 = ((w2a << 2) & 0xCCCCCCCCu) | (w2b & 0x33333333u);
+  const uint32_t O2 = (w2a & 0xCCCCCCCCu) | ((w2b >> 2) & 0x33333333u);
+  const uint32_t m4 = m0 - 0x10001000u;   // exponent field - 4 in both halves: p = 4
+#pragma unroll
+  for (int s = 0; s < 2; ++s) {
+    const uint32_t S1 = s ? O1 : E1, S2 = s ? O2 : E2;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      // byte 2h (outputs 8h+s, 8h+s+2) and byte 2h+1 (8h+s+4, 8h+s+6) of each
+      // channel, channel 1 in the low half and channel 2 in the high half
+      const uint32_t lo = __builtin_amdgcn_perm(S2, S1, h ? 0x0C060C02u : 0x0C040C00u);
+      const uint32_t hi = __builtin_amdgcn_perm(S2, S1, h ? 0x0C070C03u : 0x0C050C01u);
+      const int e = 8 * h + s;
+      acc[e] = dot2((lo & 0x000F000Fu) | m0, xp, acc[e]);
+      acc[e + 2] = dot2((lo & 0x00F000F0u) | m4, xp, acc[e + 2]);
+      acc[e + 4] = dot2((hi & 0x000F000Fu) | m0, xp, acc[e + 4]);
+      acc[e + 6] = dot2((hi & 0x00F000F0u) | m4, xp, acc[e + 6]);
+    }
+  }
+}
+
+// Offset of output e in a double unit relative to the p = 0 offset summed per
+// unit: its field sits at p = 0 or p = 4.
+__device__ __forceinline__ float double_offset_factor(int e) {
+  return ((e >> 1) & 1) ? 0.0625f : 1.0f;
+}
+
+template <int LPR, int PB, int D, int kThreads>
+__global__ __launch_bounds__(kThreads) void k_vmm_pp(
+    const uint8_t* __restrict__ codes, const uint16_t* __restrict__ scales,
+    const uint16_t* __restrict__ x, const uint8_t* __restrict__ lm, float* __restrict__ y,
+    Layer L, int gw, int fused, Thresholds th, uint8_t* __restrict__ lm_out) {
+  constexpr int T = LPR * 16;            // outputs of the tile
+  constexpr int PLANE = T / 4;           // bytes of one plane row
+  constexpr int kLaneGroups = kThreads / LPR;
+  constexpr int kWaves = kThreads / 64;
+  constexpr int kSlots = kLaneGroups * PB;   // units per batch
+
+  __shared__ __align__(16) uint32_t s_units[kPPMaxGW][kPPMaxUnits][8];
+  __shared__ __align__(16) uint32_t s_empty[kSlots][8];   // one all-empty batch
+  __shared__ int s_nbd[kPPMaxGW], s_nb[kPPMaxGW];         // double batches, all batches
+  __shared__ float s_beta[kPPMaxGW];
+  __shared__ __align__(16) uint16_t s_scale[kPPMaxGW][T];
+  __shared__ __align__(16) float s_red[kWaves][T];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int t = blockIdx.x % L.tiles;
+  const int g0 = (blockIdx.x / L.tiles) * gw;
+  const int ng = min(gw, L.groups - g0);
+  const int n_top = L.n_levels - 1;
+  const int lg = tid / LPR, li = tid % LPR;
+
+  // ---- prologue: one wave per group, lane l grades rows 2l and 2l+1 and
+  // writes its items straight into the group's unit list at ballot prefix
+  // positions.  Doubles: item i -> unit i/2, channel slot i%2.  Singles: item
+  // i -> unit (doubles padded) + i/4, pair (i/2)%2, channel slot i%2.
+  for (int gg = wave; gg < ng; gg += kWaves) {
+    const int g = g0 + gg;
+    const int r0 = 2 * lane;
+    const int k0 = g * kGroup + r0;
+    {   // this group's scales for the tile: T fp16 = 64 lanes x T/64 halves
+      constexpr int H = T / 64;
+      const uint16_t* sp = scales + (size_t)g * L.N + (size_t)t * T + lane * H;
+      if constexpr (H == 4) {
+        *(uint2*)&s_scale[gg][lane * H] = *(const uint2*)sp;
+      } else {
+#pragma unroll
+        for (int c = 0; c < H / 8; ++c) *(uint4*)&s_scale[gg][lane * H + 8 * c] = *(const uint4*)(sp + 8 * c);
+      }
+    }
+    const uint8_t* lmsrc = fused ? (const uint8_t*)x : lm;   // in fused mode the read is ignored
+    const uint32_t xx = *(const uint32_t*)(x + k0);
+    const uint16_t ll = *(const uint16_t*)(lmsrc + k0);
+    const float fa = h2f((uint16_t)(xx & 0xFFFFu)), fb = h2f((uint16_t)(xx >> 16));
+    int la, lb;
+    if (fused) {
+      la = 0;
+      lb = 0;
+      const float aa = fabsf(fa), ab = fabsf(fb);
+      for (int j = 0; j < th.n; ++j) {
+        la += aa >= th.theta[j] ? 1 : 0;
+        lb += ab >= th.theta[j] ? 1 : 0;
+      }
+      if (lm_out && t == 0) *(uint16_t*)(lm_out + k0) = (uint16_t)(la | (lb << 8));
+    } else {
+      la = min((int)(ll & 0xFFu), n_top);
+      lb = min((int)(ll >> 8), n_top);
+    }
+    const int da = level_planes(L.planes_packed, la), db = level_planes(L.planes_packed, lb);
+    const float beta = (la ? fa * phi_minus_offset(2 * da) : 0.0f) + (lb ? fb * phi_minus_offset(2 * db) : 0.0f);
+    const int nda = da >> 1, ndb = db >> 1;      // doubles of each row
+    const int nsa = da & 1, nsb = db & 1;        // singles of each row
+    const int nd = nda + ndb, ns = nsa + nsb;
+    int dpos = 0, dtot = 0, spos = 0, stot = 0;
+#pragma unroll
+    for (int q = 1; q <= 4; ++q) {
+      dpos += lanes_below(nd >= q);
+      dtot += lanes_total(nd >= q);
+    }
+#pragma unroll
+    for (int q = 1; q <= 2; ++q) {
+      spos += lanes_below(ns >= q);
+      stot += lanes_total(ns >= q);
+    }
+    const int n_du = (dtot + 1) >> 1, n_su = (stot + 3) >> 2;
+    const int pad_du = (n_du + kSlots - 1) / kSlots * kSlots;
+    int pad_su = (n_su + kSlots - 1) / kSlots * kSlots;
+    if (pad_du + pad_su == 0) pad_su = kSlots;   // an empty group still gets one batch
+    uint32_t* U = &s_units[gg][0][0];
+    const uint32_t xa = xx & 0xFFFFu, xb = xx >> 16;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      if (q >= nd) break;
+      const bool ra = q < nda;
+      const int j = 2 * (ra ? q : q - nda) + 1;               // first plane of the pair
+      const uint32_t off = (uint32_t)((k0 + (ra ? 0 : 1)) * T + (j - 1) * PLANE);
+      const int i = dpos + q, u = i >> 1, h = i & 1;
+      U[u * 8 + h] = off;
+      U[u * 8 + 4 + h] = off + PLANE;
+      reinterpret_cast<uint16_t*>(&U[u * 8 + 2])[h] = (uint16_t)((31 - 2 * j) << 10);
+      reinterpret_cast<uint16_t*>(&U[u * 8 + 3])[h] = (uint16_t)(ra ? xa : xb);
+    }
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      if (q >= ns) break;
+      const bool ra = (q == 0) && nsa;
+      const int j = ra ? da : db;                             // the odd last plane
+      const uint32_t off = (uint32_t)((k0 + (ra ? 0 : 1)) * T + (j - 1) * PLANE);
+      const int i = spos + q, u = pad_du + (i >> 2), sub = (i >> 1) & 1, h = i & 1;
+      U[u * 8 + 4 * sub + h] = off;
+      reinterpret_cast<uint16_t*>(&U[u * 8 + 4 * sub + 2])[h] = (uint16_t)((29 - 2 * j) << 10);
+      reinterpret_cast<uint16_t*>(&U[u * 8 + 4 * sub + 3])[h] = (uint16_t)(ra ? xa : xb);
+    }
+    // empty items up to whole batches: offset 0 (the tile's first row, in
+    // bounds), zero coefficient, a finite exponent word
+    for (int i = dtot + lane; i < 2 * pad_du; i += 64) {
+      const int u = i >> 1, h = i & 1;
+      U[u * 8 + h] = 0u;
+      U[u * 8 + 4 + h] = 0u;
+      reinterpret_cast<uint16_t*>(&U[u * 8 + 2])[h] = (uint16_t)(27 << 10);
+      reinterpret_cast<uint16_t*>(&U[u * 8 + 3])[h] = 0;
+    }
+    for (int i = stot + lane; i < 4 * pad_su; i += 64) {
+      const int u = pad_du + (i >> 2), sub = (i >> 1) & 1, h = i & 1;
+      U[u * 8 + 4 * sub + h] = 0u;
+      reinterpret_cast<uint16_t*>(&U[u * 8 + 4 * sub + 2])[h] = (uint16_t)(27 << 10);
+      reinterpret_cast<uint16_t*>(&U[u * 8 + 4 * sub + 3])[h] = 0;
+    }
+    const float bs = wave_sum_dpp(beta);
+    if (lane == 0) {
+      s_beta[gg] = bs;
+      s_nbd[gg] = pad_du / kSlots;
+      s_nb[gg] = (pad_du + pad_su) / kSlots;
+    }
+  }
+  for (int i = tid; i < kSlots * 8; i += kThreads) {
+    const int w = i % 8;
+    (&s_empty[0][0])[i] = (w == 2 || w == 6) ? ((27u << 10) | (27u << 26)) : 0u;
+  }
+  __syncthreads();
+
+  // ---- main loop: lane group lg takes units lg, lg + kLaneGroups, ... of
+  // each batch; the (group, batch) sequence runs through four register sets,
+  // three batches in flight while one is consumed.
+  const uint8_t* tile = codes + (size_t)t * L.K * T;
+  const uint32_t li4 = (uint32_t)li * 4u;
+  float yp[16], acc[16], off_d = 0.0f, off_s = 0.0f;
+#pragma unroll
+  for (int e = 0; e < 16; ++e) yp[e] = acc[e] = 0.0f;
+
+  struct Batch {
+    uint32_t w[PB][4];     // plane dwords: descriptor words 0, 1, 4, 5
+    uint32_t e[PB][4];     // descriptor words 2, 3, 6, 7
+  };
+  int bstart[kPPMaxGW + 1], bdbl[kPPMaxGW];
+  bstart[0] = 0;
+#pragma unroll
+  for (int gg = 0; gg < kPPMaxGW; ++gg) {
+    bstart[gg + 1] = bstart[gg] + (gg < ng ? s_nb[gg] : 0);
+    bdbl[gg] = gg < ng ? s_nbd[gg] : 0;
+  }
+  const int nbt = bstart[kPPMaxGW];
+  auto group_of = [&](int b) {
+    int gg = 0;
+#pragma unroll
+    for (int k = 1; k < kPPMaxGW; ++k) gg += (b >= bstart[k]) ? 1 : 0;
+    return gg;
+  };
+  // Issue batch b (b >= nbt reads the all-empty batch): no test, no branch.
+  auto fetch = [&](Batch& B, int b) {
+    const int gg = group_of(b);
+    const int u0 = (b - bstart[gg]) * kSlots;
+    const uint32_t* base = b < nbt ? s_units[gg][u0] : s_empty[0];
+#pragma unroll
+    for (int q = 0; q < PB; ++q) {
+      const uint32_t* src = base + (lg + kLaneGroups * q) * 8;
+      const uint4 a = *(const uint4*)src;
+      const uint4 c = *(const uint4*)(src + 4);
+      B.e[q][0] = a.z;
+      B.e[q][1] = a.w;
+      B.e[q][2] = c.z;
+      B.e[q][3] = c.w;
+      B.w[q][0] = __builtin_nontemporal_load((const uint32_t*)(tile + (a.x + li4)));
+      B.w[q][1] = __builtin_nontemporal_load((const uint32_t*)(tile + (a.y + li4)));
+      B.w[q][2] = __builtin_nontemporal_load((const uint32_t*)(tile + (c.x + li4)));
+      B.w[q][3] = __builtin_nontemporal_load((const uint32_t*)(tile + (c.y + li4)));
+    }
+  };
+  auto consume = [&](const Batch& B, int b) {
+    const int gg = group_of(b);
+    const bool dbl = b < nbt && (b - bstart[gg]) < bdbl[gg];
+    if (dbl) {
+#pragma unroll
+      for (int q = 0; q < PB; ++q) {
+        off_d = dot2(B.e[q][0], B.e[q][1], off_d);
+        consume_double(B.w[q][0], B.w[q][2], B.w[q][1], B.w[q][3], B.e[q][0], B.e[q][1], acc);
+      }
+    } else {
+      float a2[1][16];
+#pragma unroll
+      for (int e = 0; e < 16; ++e) a2[0][e] = acc[e];
+#pragma unroll
+      for (int q = 0; q < PB; ++q) {
+        const uint32_t xp0[1] = {B.e[q][1]}, xp1[1] = {B.e[q][3]};
+        off_s = dot2(B.e[q][0], B.e[q][1], off_s);
+        off_s = dot2(B.e[q][2], B.e[q][3], off_s);
+        consume_pair<1, 16>(B.w[q][0], B.w[q][1], B.e[q][0], xp0, a2, 0);
+        consume_pair<1, 16>(B.w[q][2], B.w[q][3], B.e[q][2], xp1, a2, 0);
+      }
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[e] = a2[0][e];
+    }
+  };
+  auto finish_group = [&](int gg) {
+    float sc[16];
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+      const uint4 v = *(const uint4*)&s_scale[gg][li * 16 + 8 * c];
+      const uint32_t ww[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+      for (int h = 0; h < 4; ++h) {
+        sc[8 * c + 2 * h] = h2f((uint16_t)(ww[h] & 0xFFFFu));
+        sc[8 * c + 2 * h + 1] = h2f((uint16_t)(ww[h] >> 16));
+      }
+    }
+    const float beta = lg == 0 ? s_beta[gg] : 0.0f;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      const float v = acc[e] - double_offset_factor(e) * off_d - offset_factor(e) * off_s;
+      yp[e] = fmaf(sc[e], v + beta, yp[e]);
+      acc[e] = 0.0f;
+    }
+    off_d = 0.0f;
+    off_s = 0.0f;
+  };
+  auto after = [&](int b) {
+    const int gg = group_of(b);
+    if (b + 1 == bstart[gg + 1]) finish_group(gg);
+  };
+
+  // D register sets; the inner loop is unrolled so each set is a fixed group
+  // of registers.  A workgroup with at most D-1 batches issues all its loads
+  // before it consumes the first batch.
+  Batch R[D];
+#pragma unroll
+  for (int i = 0; i < D - 1; ++i) fetch(R[i], i);
+  for (int b = 0; b < nbt; b += D) {
+#pragma unroll
+    for (int i = 0; i < D; ++i) {
+      fetch(R[(i + D - 1) % D], b + i + D - 1);
+      consume(R[i], b + i);
+      after(b + i);
+      if (b + i + 1 >= nbt) goto loop_done;
+    }
+  }
+loop_done:
+
+  // ---- reduce: lane groups of a wave by lane swaps, waves through LDS, then
+  // one atomic add per output
+#pragma unroll
+  for (int e = 0; e < 16; ++e) yp[e] = lane_group_sum<LPR>(yp[e]);
+  if (lane < LPR) {
+#pragma unroll
+    for (int c = 0; c < 4; ++c)
+      *(float4*)&s_red[wave][li * 16 + 4 * c] = make_float4(yp[4 * c], yp[4 * c + 1], yp[4 * c + 2], yp[4 * c + 3]);
+  }
+  __syncthreads();
+  for (int o = tid; o < T; o += kThreads) {
+    float v = 0.0f;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) v += s_red[w][o];
+    atomicAdd(&y[(size_t)t * T + o], v);
+  }
+}
+
+template <int LPR>
+void launch_pp(dim3 grid, hipStream_t s, const void* codes, const void* scales, const void* x,
+               const uint8_t* lm, float* y, const Layer& L, int gw, int fused,
+               const Thresholds& th, uint8_t* lm_out) {
+  hipLaunchKernelGGL((k_vmm_pp<LPR, 2, GRINQH_PP_DEPTH, 256>), grid, dim3(256), 0, s, (const uint8_t*)codes,
+                     (const uint16_t*)scales, (const uint16_t*)x, lm, y, L, gw, fused, th, lm_out);
+}
+
+}  // namespace
+
+bool vmm_pp_supported(const Layer& L, int B) {
+  // byte offsets inside a tile are 32-bit
+  return B == 1 && L.u == 2 && (L.T == 256 || L.T == 512 || L.T == 1024) &&
+         (long long)L.K * L.T < (1ll << 31);
+}
+
+int launch_vmm_pp(const Layer& L, const void* codes, const void* scales, const void* x,
+                  const uint8_t* level_map, const Thresholds* th, uint8_t* level_map_out,
+                  float* y, hipStream_t s) {
+  int gw = (int)(((long)L.tiles * L.groups) / 512);
+  gw = gw < 1 ? 1 : (gw > kPPMaxGW ? kPPMaxGW : gw);
+  if (const char* env = getenv("GRINQH_VMM_GW")) {
+    const int v = atoi(env);
+    if (v >= 1 && v <= kPPMaxGW) gw = v;
+  }
+  const dim3 grid((unsigned)(L.tiles * ((L.groups + gw - 1) / gw)));
+  Thresholds none{};
+  const Thresholds& tt = th ? *th : none;
+  const int fused = th != nullptr;
+  if (L.T == 256) launch_pp<16>(grid, s, codes, scales, x, level_map, y, L, gw, fused, tt, level_map_out);
+  else if (L.T == 512) launch_pp<32>(grid, s, codes, scales, x, level_map, y, L, gw, fused, tt, level_map_out);
+  else launch_pp<64>(grid, s, codes, scales, x, level_map, y, L, gw, fused, tt, level_map_out);
+  return check_launch("vmm (plane pairs)");
+}
+
+}  // namespace grinqh

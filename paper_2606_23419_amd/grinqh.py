@@ -29,8 +29,8 @@ MAX_LEVELS = 9
 
 EXPORTED = (
     "grinqh_resolve_desc", "grinqh_packed_bytes", "grinqh_pack", "grinqh_topk_counts",
-    "grinqh_workspace_bytes", "grinqh_assign", "grinqh_vmm", "grinqh_vmm_threshold",
-    "grinqh_last_error",
+    "grinqh_workspace_bytes", "grinqh_calibrate", "grinqh_assign", "grinqh_vmm",
+    "grinqh_vmm_threshold", "grinqh_last_error",
 )
 
 
@@ -69,6 +69,7 @@ def _load():
         "grinqh_pack": [dp, ctypes.c_int, vp, vp, vp, vp, vp],
         "grinqh_topk_counts": [i32, i32, ctypes.POINTER(i32), ctypes.POINTER(i32)],
         "grinqh_workspace_bytes": [dp, i32, ctypes.POINTER(sz)],
+        "grinqh_calibrate": [dp, vp, i32, ctypes.POINTER(i32), vp, vp, vp],
         "grinqh_assign": [dp, ctypes.c_int, vp, i32, ctypes.POINTER(ctypes.c_float),
                           ctypes.POINTER(i32), vp, vp, sz, vp],
         "grinqh_vmm": [dp, vp, vp, vp, vp, i32, vp, i32, vp, sz, vp],
@@ -195,6 +196,27 @@ def grinqh_pack(desc: LayerDesc, W=None, codes=None, scales=None, out_codes=None
 def _floats(vals):
     vals = [float(v) for v in vals]
     return (ctypes.c_float * max(1, len(vals)))(*vals)
+
+
+def grinqh_calibrate(desc: LayerDesc, x, p_bp, per_sample=None, theta=None, stream=None):
+    """Thresholds theta_1..theta_n (fp32 device tensor) calibrated on the fp16
+    samples x [S, K] for the precision distribution p_bp (basis points)."""
+    torch = _torch()
+    rd = grinqh_resolve_desc(desc)
+    if x.dim() == 1:
+        x = x.view(1, -1)
+    S = int(x.shape[0])
+    n = rd.n_levels - 1
+    xp = _dev(x, torch.float16, "x", (S, rd.K))
+    if per_sample is None:
+        per_sample = torch.empty((S, n), dtype=torch.float64, device=x.device)
+    if theta is None:
+        theta = torch.empty((n,), dtype=torch.float32, device=x.device)
+    pp = _dev(per_sample, torch.float64, "per_sample", (S, n))
+    tp = _dev(theta, torch.float32, "theta", (n,))
+    arr = (ctypes.c_int32 * len(p_bp))(*[int(v) for v in p_bp])
+    _check(lib.grinqh_calibrate(ctypes.byref(rd), xp, S, arr, pp, tp, _stream(stream)))
+    return theta
 
 
 def grinqh_assign(desc: LayerDesc, x, mode: int, thresholds=None, counts=None, out=None,

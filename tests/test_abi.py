@@ -140,6 +140,23 @@ def test_assign_validation(g):
     assert A(ctypes.byref(big), 1, FAKE, 1, None, _cn([0, 128 * 129]), FAKE, None, 0, None) == -2
 
 
+def test_calibrate_validation(g):
+    d = g.make_desc(256, 512, (0, 2, 4, 8))
+    C = g.lib.grinqh_calibrate
+    p = _cn([2000, 3000, 3000, 2000])
+    assert C(ctypes.byref(d), None, 1, p, FAKE, FAKE, None) == -1
+    assert C(ctypes.byref(d), FAKE, 0, p, FAKE, FAKE, None) == -1
+    assert C(ctypes.byref(d), FAKE, 70000, p, FAKE, FAKE, None) == -1
+    assert C(ctypes.byref(d), FAKE, 1, _cn([2000, 3000, 3000, 1999]), FAKE, FAKE, None) == -1
+    assert C(ctypes.byref(d), FAKE, 1, _cn([-1, 3000, 3000, 4001]), FAKE, FAKE, None) == -1
+    assert C(ctypes.byref(d), FAKE, 1, p, ctypes.c_void_p(0x1004), FAKE, None) == -1
+    assert C(ctypes.byref(d), FAKE, 1, p, FAKE, None, None) == -1
+    assert C(ctypes.byref(d), FAKE, 1, None, FAKE, FAKE, None) == -1
+    big = g.make_desc(128 * 129, 512, (0, 8))
+    assert C(ctypes.byref(big), FAKE, 1, _cn([5000, 5000]), FAKE, FAKE, None) == -2
+    assert "K <= 16384" in g.grinqh_last_error()
+
+
 def test_vmm_validation(g):
     d = g.make_desc(256, 512, (0, 2, 4, 8))
     V = g.lib.grinqh_vmm

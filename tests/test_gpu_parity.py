@@ -251,6 +251,47 @@ def test_vmm_threshold_fused(g, torch, levels):
     assert normwise(_host(y), ref) <= TOL
 
 
+# ------------------------------------------------------- calibration ----
+@pytest.mark.parametrize("K", [128, 1152, 4096, 14336])
+def test_calibrate_matches_oracle(g, torch, K):
+    levels = inputs.LEVELS_B
+    d = g.make_desc(K, 1024, levels)
+    S = 12
+    x = inputs.activations_t3(K, S, 67, K)
+    rng = np.random.default_rng(K)
+    x[3] = rng.integers(-3, 4, K).astype(np.float16)          # heavy ties
+    x[5] = np.float16(0.5)                                     # one value
+    samples = [np.abs(r.astype(np.float64)) for r in x]
+    budgets = list(inputs.BUDGETS[levels].values()) + [(0, 0, 0, 0, 10000), (10000, 0, 0, 0, 0),
+                                                       (1, 1, 1, 1, 9996)]
+    for p in budgets:
+        th = _host(g.grinqh_calibrate(d, _dev(torch, x), p))
+        ref = orc.calibrate_thresholds(samples, p)
+        assert np.array_equal(th, ref), (K, p, th, ref)
+
+
+def test_calibrated_threshold_path_hits_budget(g, torch):
+    # calibrate on one set of tokens, grade held-out tokens inside the VMM
+    levels = inputs.LEVELS_B
+    K, N = 4096, 1024
+    L = Layer(g, torch, K, N, levels, cfg=68)
+    calib = inputs.activations_t3(K, 64, 68, 1)
+    test = inputs.activations_t3(K, 8, 68, 2)
+    p = inputs.BUDGETS[levels][4]
+    th = _host(g.grinqh_calibrate(L.desc, _dev(torch, calib), p))
+    lm_out = torch.zeros((8, K), dtype=torch.uint8, device="cuda")
+    xd = _dev(torch, test)
+    ys = [g.grinqh_vmm_threshold(L.desc, L.pc, L.ps, xd[t:t + 1], th, level_map_out=lm_out[t:t + 1])
+          for t in range(8)]
+    torch.cuda.synchronize()
+    lm = orc.assign_threshold(test, th)
+    assert np.array_equal(_host(lm_out), lm)
+    y = np.concatenate([_host(v) for v in ys])
+    assert normwise(y, orc.vmm_batch(L.codes, L.scales, test, lm, levels)) <= TOL
+    achieved = float(np.asarray(levels)[lm].mean())
+    assert abs(achieved - 4.0) < 0.25, achieved
+
+
 # ------------------------------------------ full-size workload shapes ----
 FULL = [
     ("cfg1 1024x1024", 1024, 1024, inputs.LEVELS_A, "t3"),
@@ -282,13 +323,16 @@ def test_full_size_pack_and_sampled_vmm(g, torch, name, K, N, levels, xkind):
         assert np.all(np.isfinite(y))
 
 
-@pytest.mark.parametrize("threads", ["256", "512"])
+@pytest.mark.parametrize("kernel", ["pp", "dot2-256", "dot2-512"])
 @pytest.mark.parametrize("gw", ["1", "2", "3", "4"])
 @pytest.mark.parametrize("tile_n", [256, 512, 1024])
-def test_vmm_groups_per_workgroup(g, torch, gw, tile_n, threads, monkeypatch):
-    # K = 1152 is 9 groups: every gw > 1 leaves a ragged last workgroup
+def test_vmm_groups_per_workgroup(g, torch, gw, tile_n, kernel, monkeypatch):
+    # K = 1152 is 9 groups: every gw > 1 leaves a ragged last workgroup.  At
+    # B = 1 the plane-pair kernel runs unless the per-plane kernel is forced.
     monkeypatch.setenv("GRINQH_VMM_GW", gw)
-    monkeypatch.setenv("GRINQH_VMM_THREADS", threads)
+    if kernel.startswith("dot2"):
+        monkeypatch.setenv("GRINQH_VMM_KERNEL", "dot2")
+        monkeypatch.setenv("GRINQH_VMM_THREADS", kernel.split("-")[1])
     levels = (0, 2, 4, 6, 8)
     K, N = 1152, 1024
     L = Layer(g, torch, K, N, levels, cfg=64, tile_n=tile_n)
@@ -300,8 +344,11 @@ def test_vmm_groups_per_workgroup(g, torch, gw, tile_n, threads, monkeypatch):
         assert normwise(y, ref) <= TOL, (gw, tile_n, B, normwise(y, ref))
 
 
-def test_vmm_precision_margin(g, torch):
+@pytest.mark.parametrize("kernel", ["pp", "dot2"])
+def test_vmm_precision_margin(g, torch, kernel, monkeypatch):
     # the contract is 1e-3; the fp32 accumulation should sit far below it
+    if kernel == "dot2":
+        monkeypatch.setenv("GRINQH_VMM_KERNEL", "dot2")
     levels = (0, 2, 4, 6, 8)
     K, N = 4096, 1024
     L = Layer(g, torch, K, N, levels, cfg=65, tile_n=256)
