@@ -84,8 +84,17 @@ __global__ __launch_bounds__(kThreads) void k_vmm_dot2(
     const int g = g0 + gg;
     const int r0 = 2 * lane;
     const int k0 = g * kGroup + r0;
-    // this group's scales for the tile go to LDS: T fp16 = 64 lanes x 4V halves
-    {
+    // x, the level map and the scales are requested together, so the
+    // prologue waits for one memory latency, not two
+    uint32_t xxs[NB];
+    uint16_t lls[NB];
+    const uint8_t* lmsrc = fused ? (const uint8_t*)x : lm;   // in fused mode the read is ignored
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+      xxs[b] = *(const uint32_t*)(x + (size_t)b * L.K + k0);
+      lls[b] = *(const uint16_t*)(lmsrc + (size_t)b * L.K + k0);
+    }
+    {   // this group's scales for the tile go to LDS: T fp16 = 64 lanes x 4V halves
       constexpr int H = T / 64;   // halves per lane: 4, 8 or 16
       const uint16_t* sp = scales + (size_t)g * L.N + (size_t)t * T + lane * H;
       if constexpr (H == 4) {
@@ -95,14 +104,8 @@ __global__ __launch_bounds__(kThreads) void k_vmm_dot2(
         for (int c = 0; c < H / 8; ++c) *(uint4*)&s_scale[gg][lane * H + 8 * c] = *(const uint4*)(sp + 8 * c);
       }
     }
-    uint32_t xxs[NB];
-    uint16_t lls[NB];
-    const uint8_t* lmsrc = fused ? (const uint8_t*)x : lm;   // in fused mode the read is ignored
 #pragma unroll
-    for (int b = 0; b < NB; ++b) {
-      xxs[b] = *(const uint32_t*)(x + (size_t)b * L.K + k0);
-      lls[b] = *(const uint16_t*)(lmsrc + (size_t)b * L.K + k0);
-    }
+    for (int b = 0; b < NB; ++b) asm volatile("" ::"v"(lls[b]));   // level-map loads issued before the wait above
     int da[NB], db[NB];
     int D0 = 0, D1 = 0;
     float beta[NB];
@@ -114,9 +117,10 @@ __global__ __launch_bounds__(kThreads) void k_vmm_dot2(
         la = 0;
         lb = 0;
         const float aa = fabsf(fa), ab = fabsf(fb);
-        for (int j = 0; j < th.n; ++j) {
-          la += aa >= th.theta[j] ? 1 : 0;
-          lb += ab >= th.theta[j] ? 1 : 0;
+#pragma unroll
+        for (int j = 0; j < kMaxLevels - 1; ++j) {   // unrolled: the thresholds are one scalar load
+          la += (j < th.n && aa >= th.theta[j]) ? 1 : 0;
+          lb += (j < th.n && ab >= th.theta[j]) ? 1 : 0;
         }
         if (lm_out && t == 0)
           *(uint16_t*)(lm_out + (size_t)b * L.K + k0) = (uint16_t)(la | (lb << 8));

@@ -35,6 +35,9 @@ namespace {
 
 using namespace vmmdev;
 
+#ifndef GRINQH_PP_PREFETCH
+#define GRINQH_PP_PREFETCH false
+#endif
 #ifndef GRINQH_PP_DEPTH
 #define GRINQH_PP_DEPTH 4
 #endif
@@ -77,7 +80,7 @@ __device__ __forceinline__ float double_offset_factor(int e) {
   return ((e >> 1) & 1) ? 0.0625f : 1.0f;
 }
 
-template <int LPR, int PB, int D, int kThreads>
+template <int LPR, int PB, int D, int kThreads, bool PREFETCH>
 __global__ __launch_bounds__(kThreads) void k_vmm_pp(
     const uint8_t* __restrict__ codes, const uint16_t* __restrict__ scales,
     const uint16_t* __restrict__ x, const uint8_t* __restrict__ lm, float* __restrict__ y,
@@ -102,6 +105,25 @@ __global__ __launch_bounds__(kThreads) void k_vmm_pp(
   const int n_top = L.n_levels - 1;
   const int lg = tid / LPR, li = tid % LPR;
 
+  // Before anything else, touch plane 1 of the first group's 128 rows, one
+  // dword per 128-byte line, so that the main loop finds these lines in L2
+  // instead of waiting a memory latency for them after the prologue.  Every
+  // channel above level 0 reads plane 1; the lines of level-0 rows are the
+  // only bytes fetched without need.  The load is written as asm so that
+  // nothing waits for it: its destination register stays live (and unread)
+  // until the single wait at the end of the kernel.  The compiler's own
+  // waits count this older load too, which only makes them stricter.
+  uint32_t pf = 0;
+  if constexpr (PREFETCH) {
+    constexpr int kLinesPerRow = PLANE >= 128 ? PLANE / 128 : 1;
+    constexpr int kRowsPerLine = PLANE >= 128 ? 1 : 128 / PLANE;
+    constexpr int kLines = kGroup * kLinesPerRow / kRowsPerLine;   // <= kThreads
+    const int i = tid % kLines;   // threads past kLines repeat a line
+    const int r = (i / kLinesPerRow) * kRowsPerLine, c = i % kLinesPerRow;
+    const uint8_t* a = codes + (size_t)t * L.K * T + (size_t)(g0 * kGroup + r) * T + c * 128;
+    asm volatile("global_load_dword %0, %1, off" : "=v"(pf) : "v"(a) : "memory");
+  }
+
   // ---- prologue: one wave per group, lane l grades rows 2l and 2l+1 and
   // writes its items straight into the group's unit list at ballot prefix
   // positions.  Doubles: item i -> unit i/2, channel slot i%2.  Singles: item
@@ -110,6 +132,11 @@ __global__ __launch_bounds__(kThreads) void k_vmm_pp(
     const int g = g0 + gg;
     const int r0 = 2 * lane;
     const int k0 = g * kGroup + r0;
+    // x, the level map and the scales are requested together, so the
+    // prologue waits for one memory latency, not two
+    const uint8_t* lmsrc = fused ? (const uint8_t*)x : lm;   // in fused mode the read is ignored
+    const uint32_t xx = *(const uint32_t*)(x + k0);
+    const uint16_t ll = *(const uint16_t*)(lmsrc + k0);
     {   // this group's scales for the tile: T fp16 = 64 lanes x T/64 halves
       constexpr int H = T / 64;
       const uint16_t* sp = scales + (size_t)g * L.N + (size_t)t * T + lane * H;
@@ -120,18 +147,17 @@ __global__ __launch_bounds__(kThreads) void k_vmm_pp(
         for (int c = 0; c < H / 8; ++c) *(uint4*)&s_scale[gg][lane * H + 8 * c] = *(const uint4*)(sp + 8 * c);
       }
     }
-    const uint8_t* lmsrc = fused ? (const uint8_t*)x : lm;   // in fused mode the read is ignored
-    const uint32_t xx = *(const uint32_t*)(x + k0);
-    const uint16_t ll = *(const uint16_t*)(lmsrc + k0);
+    asm volatile("" ::"v"(ll));   // the level-map load is issued before the wait above
     const float fa = h2f((uint16_t)(xx & 0xFFFFu)), fb = h2f((uint16_t)(xx >> 16));
     int la, lb;
     if (fused) {
       la = 0;
       lb = 0;
       const float aa = fabsf(fa), ab = fabsf(fb);
-      for (int j = 0; j < th.n; ++j) {
-        la += aa >= th.theta[j] ? 1 : 0;
-        lb += ab >= th.theta[j] ? 1 : 0;
+#pragma unroll
+      for (int j = 0; j < kMaxLevels - 1; ++j) {   // unrolled: the thresholds are one scalar load
+        la += (j < th.n && aa >= th.theta[j]) ? 1 : 0;
+        lb += (j < th.n && ab >= th.theta[j]) ? 1 : 0;
       }
       if (lm_out && t == 0) *(uint16_t*)(lm_out + k0) = (uint16_t)(la | (lb << 8));
     } else {
@@ -343,13 +369,14 @@ loop_done:
     for (int w = 0; w < kWaves; ++w) v += s_red[w][o];
     atomicAdd(&y[(size_t)t * T + o], v);
   }
+  if constexpr (PREFETCH) asm volatile("s_waitcnt vmcnt(0)" : "+v"(pf)::"memory");
 }
 
 template <int LPR>
 void launch_pp(dim3 grid, hipStream_t s, const void* codes, const void* scales, const void* x,
                const uint8_t* lm, float* y, const Layer& L, int gw, int fused,
                const Thresholds& th, uint8_t* lm_out) {
-  hipLaunchKernelGGL((k_vmm_pp<LPR, 2, GRINQH_PP_DEPTH, 256>), grid, dim3(256), 0, s, (const uint8_t*)codes,
+  hipLaunchKernelGGL((k_vmm_pp<LPR, 2, GRINQH_PP_DEPTH, 256, GRINQH_PP_PREFETCH>), grid, dim3(256), 0, s, (const uint8_t*)codes,
                      (const uint16_t*)scales, (const uint16_t*)x, lm, y, L, gw, fused, th, lm_out);
 }
 
