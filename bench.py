@@ -62,6 +62,12 @@ WORKLOADS = {
                            ref=[]),
     "single-1024": dict(cfg=1, levels=inputs.LEVELS_A, budget=4,
                         layers=[("w", 1024, 1024, 0, "t3")], ref=[]),
+    # the whole decode step: 32 layers, merged projections, batch 1, 2 or 4
+    "llama3-8b-decode": dict(cfg=5, levels=inputs.LEVELS_B, budget=4,
+                             layers=[("qkv", 4096, 6144, 0, "t3"), ("o", 4096, 4096, 1, "t3"),
+                                     ("gate_up", 4096, 28672, 2, "t3"),
+                                     ("down", 14336, 4096, 3, "swiglu")],
+                             ref=[], n_layers=32),
 }
 
 
@@ -118,6 +124,8 @@ def parse():
     ap.add_argument("--assign", default="threshold", choices=("threshold", "topk"))
     ap.add_argument("--budget", type=int, default=None, help="override the average-bit budget")
     ap.add_argument("--tokens", type=int, default=256)
+    ap.add_argument("--batch", type=int, default=1, help="tokens per VMM call (decode workload)")
+    ap.add_argument("--n-layers", type=int, default=0, help="decoder layers (decode workload)")
     ap.add_argument("--tile-n", type=int, default=0)
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
     ap.add_argument("--vmm-only-reps", type=int, default=5)
@@ -137,6 +145,16 @@ def bytes_required(level_map: np.ndarray, level_bits, K: int, N: int, reads_map:
     code = bits.sum(axis=1) * N // 8
     active_groups = (level_map.reshape(level_map.shape[0], K // 128, 128) > 0).any(axis=2).sum(axis=1)
     return code + active_groups * N * 2 + 2 * K + 4 * N + (K if reads_map else 0)
+
+
+def bytes_required_batch(level_map: np.ndarray, level_bits, K: int, N: int, reads_map: bool) -> int:
+    """Algorithmic bytes of one VMM over B tokens (level_map [B, K]): each
+    channel's code prefix to the deepest level over the tokens, the scales of
+    groups any token uses, and x, y (and level maps) per token."""
+    B = level_map.shape[0]
+    bits = np.asarray(level_bits, dtype=np.int64)[level_map.astype(np.int64)].max(axis=0)   # [K]
+    active_groups = int((level_map.reshape(B, K // 128, 128) > 0).any(axis=(0, 2)).sum())
+    return int(bits.sum()) * N // 8 + active_groups * N * 2 + B * (2 * K + 4 * N + (K if reads_map else 0))
 
 
 def make_inputs(wl, tokens: int, seed_base: int):
@@ -181,6 +199,123 @@ def cpu_baseline(wl, p_bp, assign: str, tokens_sample: int):
                       f"same workload, numpy float64, 1 thread; {dt:.1f} s"}
 
 
+def run_decode(args, torch, g):
+    """The full decode step: n_layers x (qkv, o, gate_up, down) at batch B.
+
+    Weights are uniform random 8-bit codes with fp16 scales, drawn on the GPU
+    from a seeded generator and packed with grinqh_pack (pre-quantised codes);
+    7 GB of fp16 weights drawn on the host would take minutes.  Every layer
+    has its own weights; the activations of each projection kind are shared
+    by the layers (they only decide which bytes are read)."""
+    dev = torch.device("cuda:0")
+    wl = WORKLOADS["llama3-8b-decode"]
+    levels, layers = wl["levels"], wl["layers"]
+    L = args.n_layers or wl["n_layers"]
+    B = args.batch
+    if not 1 <= B <= 4:
+        print("--batch must be 1..4", file=sys.stderr)
+        sys.exit(2)
+    budget = args.budget if args.budget is not None else wl["budget"]
+    p_bp = inputs.BUDGETS[levels][budget]
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(5)
+    descs = {name: g.grinqh_resolve_desc(g.make_desc(K, N, levels, tile_n=args.tile_n))
+             for name, K, N, _, _ in layers}
+    weights = []
+    for li in range(L):
+        per = {}
+        for name, K, N, _, _ in layers:
+            codes = torch.randint(0, 256, (N, K), dtype=torch.uint8, device=dev, generator=gen)
+            sc = (torch.rand((N, K // 128), device=dev, generator=gen) * 4e-4 + 1e-4).half()
+            per[name] = g.grinqh_pack(descs[name], codes=codes, scales=sc)
+            del codes, sc
+        weights.append(per)
+    torch.cuda.synchronize()
+    xs = {k: torch.from_numpy(v[:B].copy()).to(dev) for k, v in make_inputs(wl, B, 100).items()}
+    calib = {k: torch.from_numpy(v).to(dev) for k, v in make_inputs(wl, CALIB_TOKENS, 200).items()}
+    desc_of = {xin: descs[name] for name, _, _, xin, _ in layers}
+    thresholds = {xin: g.grinqh_calibrate(desc_of[xin], calib[xin], p_bp).cpu().numpy() for xin in xs}
+    counts = {xin: g.grinqh_topk_counts(int(xs[xin].shape[1]), p_bp) for xin in xs}
+    lm = {xin: torch.zeros((B, int(x.shape[1])), dtype=torch.uint8, device=dev) for xin, x in xs.items()}
+    ys = {name: torch.zeros((B, N), dtype=torch.float32, device=dev) for name, _, N, _, _ in layers}
+
+    def step(mode):
+        for li in range(L):
+            w = weights[li]
+            for name, K, N, xin, _ in layers:
+                if mode == "threshold":
+                    g.grinqh_vmm_threshold(descs[name], w[name][0], w[name][1], xs[xin], thresholds[xin],
+                                           y=ys[name], level_map_out=lm[xin] if li == 0 else None)
+                else:
+                    g.grinqh_assign(descs[name], xs[xin], g.GRINQH_ASSIGN_TOPK, counts=counts[xin],
+                                    out=lm[xin])
+                    g.grinqh_vmm(descs[name], w[name][0], w[name][1], xs[xin], lm[xin], y=ys[name])
+
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    out_modes = {}
+    for mode in (args.assign, "topk" if args.assign == "threshold" else "threshold"):
+        with torch.cuda.stream(s):
+            step(mode)
+        torch.cuda.synchronize()
+        eager = {n: y.clone() for n, y in ys.items()}
+        lm_host = {xin: m.cpu().numpy() for xin, m in lm.items()}
+        gr = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(gr, stream=s):
+            step(mode)
+        with torch.cuda.stream(s):
+            gr.replay()
+        torch.cuda.synchronize()
+        for n, y in ys.items():
+            err = float((y - eager[n]).abs().max() / eager[n].abs().max())
+            if not err <= 1e-5:
+                raise RuntimeError(f"graph replay of {n} ({mode}) differs from the eager step ({err:.2e})")
+        step_bytes = L * sum(bytes_required_batch(lm_host[xin], levels, K, N, mode == "topk")
+                             for _, K, N, xin, _ in layers)
+        reps = args.steps if mode == args.assign else 3
+        with torch.cuda.stream(s):
+            for _ in range(args.warmup):
+                gr.replay()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        with torch.cuda.stream(s):
+            a.record(s)
+            for _ in range(reps):
+                gr.replay()
+            b.record(s)
+        torch.cuda.synchronize()
+        ms = a.elapsed_time(b) / reps
+        out_modes[mode] = {"ms_per_step": round(ms, 4), "step_bytes": step_bytes,
+                           "value": round(step_bytes / (ms * 1e-3) / 1e9, 2),
+                           "achieved_avg_bits": {f"input{xin}": round(float(np.asarray(levels)[m].mean()), 4)
+                                                 for xin, m in lm_host.items()}}
+        del gr
+    main = out_modes[args.assign]
+    other = "topk" if args.assign == "threshold" else "threshold"
+    n_vmm = L * len(layers)
+    packed_gb = sum(w[n][0].numel() + 2 * w[n][1].numel() for w in weights for n in w) / 1e9
+    out = {
+        "metric": "µs per decode VMM and effective HBM GB/s (% of peak) vs avg bits, batch 1",
+        "value": main["value"], "unit": "GB/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": main["ms_per_step"], "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "u8 codes, fp16 x, f32 accumulate",
+        "data": "synthetic (uniform random 8-bit codes and fp16 scales; Student-t(3) activations "
+                "with 1% x20 outlier channels; SiLU(g)*u for down projections)",
+        "config": {"workload": "llama3-8b-decode", "decoder_layers": L, "batch": B,
+                   "layers": {n: [K, N] for n, K, N, _, _ in layers}, "levels": list(levels),
+                   "budget_bits": budget, "assignment": args.assign, "P_bp": list(p_bp),
+                   "packed_weights_GB": round(packed_gb, 3), "achieved_avg_bits": main["achieved_avg_bits"]},
+        "tokens_per_s": round(B / (main["ms_per_step"] * 1e-3), 1),
+        "ms_per_token_step": main["ms_per_step"],
+        "us_per_vmm": round(main["ms_per_step"] * 1e3 / n_vmm, 3),
+        "roofline": {"bound": "hbm", "achieved": main["value"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(main["value"] / HBM_PEAK_GBS, 4), "traffic": None},
+        "other_assignment": dict(assignment=other, **{k: v for k, v in out_modes[other].items()
+                                                       if k != "step_bytes"}),
+    }
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse()
     if args.vmm_source_sha:
@@ -196,6 +331,9 @@ def main():
 
     import torch
     from paper_2606_23419_amd import grinqh as g
+
+    if args.workload == "llama3-8b-decode":
+        return run_decode(args, torch, g)
 
     dev = torch.device("cuda:0")
     wl = WORKLOADS[args.workload]

@@ -117,7 +117,7 @@ int launch_vmm(const Layer& L, const void* codes, const void* scales, const void
   const bool want_dot2 = force && force[0] == 'd', want_v0 = force && force[0] == 'v';
   if (!want_dot2 && !want_v0 && vmm_pp_supported(L, B))
     return launch_vmm_pp(L, codes, scales, x, level_map, th, level_map_out, y, s);
-  if (!want_v0 && vmm_dot2_supported(L) && !(L.T == 1024 && B > 2))
+  if (!want_v0 && vmm_dot2_supported(L))
     return launch_vmm_dot2(L, codes, scales, x, level_map, th, level_map_out, B, y, s);
   // about 512 workgroups per token over the whole chip
   int ksplit = (512 + L.tiles - 1) / L.tiles;

@@ -364,8 +364,7 @@ void launch_one(dim3 grid, hipStream_t s, const void* codes, const void* scales,
 }  // namespace
 
 // Tiles of 256, 512 or 1024 outputs: one dword (16 outputs) per lane and
-// plane row, so 16, 32 or 64 lanes cover a plane row.  B > 2 keeps the tile
-// at 512 or below (LDS of the cross-wave reduction).
+// plane row, so 16, 32 or 64 lanes cover a plane row.
 bool vmm_dot2_supported(const Layer& L) {
   return L.u == 2 && (L.T == 256 || L.T == 512 || L.T == 1024);
 }
@@ -405,7 +404,7 @@ int launch_vmm_dot2(const Layer& L, const void* codes, const void* scales, const
   }
   GRINQH_DOT2_CASE(256, 16, 1) GRINQH_DOT2_CASE(256, 16, 2) GRINQH_DOT2_CASE(256, 16, 3) GRINQH_DOT2_CASE(256, 16, 4)
   GRINQH_DOT2_CASE(512, 32, 1) GRINQH_DOT2_CASE(512, 32, 2) GRINQH_DOT2_CASE(512, 32, 3) GRINQH_DOT2_CASE(512, 32, 4)
-  GRINQH_DOT2_CASE(1024, 64, 1) GRINQH_DOT2_CASE(1024, 64, 2)
+  GRINQH_DOT2_CASE(1024, 64, 1) GRINQH_DOT2_CASE(1024, 64, 2) GRINQH_DOT2_CASE(1024, 64, 3) GRINQH_DOT2_CASE(1024, 64, 4)
 #undef GRINQH_DOT2_CASE
   return fail(GRINQH_EUNSUPPORTED, "dot2 VMM: no kernel for tile %d, B=%d", L.T, B);
 }
