@@ -68,7 +68,14 @@ WORKLOADS = {
                                      ("gate_up", 4096, 28672, 2, "t3"),
                                      ("down", 14336, 4096, 3, "swiglu")],
                              ref=[], n_layers=32),
+    # prefill of one decoder layer: M prompt tokens, every channel at 8 bits
+    "llama3-8b-prefill": dict(cfg=6, levels=inputs.LEVELS_B, budget=8,
+                              layers=[("qkv", 4096, 6144, 0, "t3"), ("o", 4096, 4096, 1, "t3"),
+                                      ("gate_up", 4096, 28672, 2, "t3"),
+                                      ("down", 14336, 4096, 3, "swiglu")],
+                              ref=[], tokens=2048),
 }
+MFMA_F16_PEAK_TFLOPS = 2500.0
 
 
 def vmm_source_sha() -> str:
@@ -126,6 +133,7 @@ def parse():
     ap.add_argument("--tokens", type=int, default=256)
     ap.add_argument("--batch", type=int, default=1, help="tokens per VMM call (decode workload)")
     ap.add_argument("--n-layers", type=int, default=0, help="decoder layers (decode workload)")
+    ap.add_argument("--prefill-tokens", type=int, default=0, help="prompt tokens M (prefill workload)")
     ap.add_argument("--tile-n", type=int, default=0)
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
     ap.add_argument("--vmm-only-reps", type=int, default=5)
@@ -316,6 +324,133 @@ def run_decode(args, torch, g):
     print(json.dumps(out), flush=True)
 
 
+def cpu_baseline_prefill(wl, tokens_sample: int):
+    """Time the oracle's prefill (float64 dequantise + dense product) on host cores."""
+    from threadpoolctl import threadpool_limits
+    from oracle import grinqh_oracle as orc
+
+    flops = 0
+    with threadpool_limits(limits=1):
+        dt = 0.0
+        for li, (name, K, N, xin, kind) in enumerate(wl["layers"]):
+            codes = inputs.random_codes(N, K, wl["cfg"], li)
+            sc = inputs.random_scales(N, K, 128, wl["cfg"], li).T.copy()
+            gen = inputs.activations_swiglu if kind == "swiglu" else inputs.activations_t3
+            x = gen(K, tokens_sample, wl["cfg"], 100 + xin)
+            t0 = time.perf_counter()
+            orc.prefill(codes, sc, x)
+            dt += time.perf_counter() - t0
+            flops += 2 * tokens_sample * K * N
+    return {"value": round(flops / dt / 1e12, 5), "unit": "TFLOP/s", "cores": 1, "kind": "oracle",
+            "sample": f"{tokens_sample} tokens x {len(wl['layers'])} projections of the same layer, "
+                      f"numpy float64 dequantise + product, 1 thread; {dt:.1f} s"}
+
+
+def run_prefill(args, torch, g):
+    """Prefill of one decoder layer: the four projections at M tokens, each
+    a grinqh_prefill launch over the packed nested weights (all 8 bits).
+
+    Weights are uniform random codes with fp16 scales drawn on the GPU and
+    packed from codes; a plain fp16 GEMM (torch.mm on the unpacked weights,
+    i.e. hipBLASLt) is timed on the same shapes as context."""
+    dev = torch.device("cuda:0")
+    wl = WORKLOADS["llama3-8b-prefill"]
+    levels, layers = wl["levels"], wl["layers"]
+    M = args.prefill_tokens or wl["tokens"]
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(6)
+    descs, packed, dense = {}, {}, {}
+    for name, K, N, _, _ in layers:
+        d = g.grinqh_resolve_desc(g.make_desc(K, N, levels, tile_n=args.tile_n))
+        codes = torch.randint(0, 256, (N, K), dtype=torch.uint8, device=dev, generator=gen)
+        sc = (torch.rand((N, K // 128), device=dev, generator=gen) * 4e-4 + 1e-4).half()
+        descs[name], packed[name] = d, g.grinqh_pack(d, codes=codes, scales=sc)
+        w = (codes.float() - 128.0) * sc.float().repeat_interleave(128, dim=1)
+        dense[name] = w.t().contiguous().half()        # [K, N], for torch.mm(x, w)
+        del codes, sc, w
+    xs = {}
+    for name, K, N, xin, kind in layers:
+        if xin not in xs:
+            x = torch.randn((M, K), device=dev, generator=gen)
+            xs[xin] = (torch.nn.functional.silu(x) * torch.randn((M, K), device=dev, generator=gen)
+                       if kind == "swiglu" else x).half()
+    ys = {name: torch.empty((M, N), dtype=torch.float32, device=dev) for name, _, N, _, _ in layers}
+    yd = {name: torch.empty((M, N), dtype=torch.float16, device=dev) for name, _, N, _, _ in layers}
+    torch.cuda.synchronize()
+
+    def ours(only=None):
+        for name, _, _, xin, _ in layers:
+            if only is None or name == only:
+                g.grinqh_prefill(descs[name], packed[name][0], packed[name][1], xs[xin], y=ys[name])
+
+    def torch_dense(only=None):
+        for name, _, _, xin, _ in layers:
+            if only is None or name == only:
+                torch.mm(xs[xin], dense[name], out=yd[name])
+
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+
+    def timed(fn, reps, warm):
+        with torch.cuda.stream(s):
+            for _ in range(warm):
+                fn()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        with torch.cuda.stream(s):
+            a.record(s)
+            for _ in range(reps):
+                fn()
+            b.record(s)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / reps
+
+    # check against the dense product on a few rows (the oracle is for the tests)
+    with torch.cuda.stream(s):
+        ours()
+        torch_dense()
+    torch.cuda.synchronize()
+    for name, _, _, xin, _ in layers:
+        rows = torch.arange(0, M, max(1, M // 8), device=dev)
+        ref = xs[xin][rows].float() @ dense[name].float()
+        err = float((ys[name][rows] - ref).abs().max() / ref.abs().max())
+        if not err <= 1e-3:
+            raise RuntimeError(f"prefill {name} differs from the dense product ({err:.2e})")
+
+    layer_flops = {name: 2 * M * K * N for name, K, N, _, _ in layers}
+    step_flops = sum(layer_flops.values())
+    ms_step = timed(ours, args.steps, args.warmup)
+    ms_dense = timed(torch_dense, max(3, args.steps), 2)
+    per_layer = {}
+    for name, K, N, _, _ in layers:
+        ms = timed(lambda: ours(name), 5, 1)
+        msd = timed(lambda: torch_dense(name), 5, 1)
+        per_layer[name] = {"K": K, "N": N, "us": round(ms * 1e3, 1),
+                           "TFLOPs": round(layer_flops[name] / (ms * 1e-3) / 1e12, 1),
+                           "torch_fp16_TFLOPs": round(layer_flops[name] / (msd * 1e-3) / 1e12, 1),
+                           "tile_n": int(descs[name].tile_n)}
+    dom = max(layers, key=lambda l: layer_flops[l[0]])[0]
+    value = step_flops / (ms_step * 1e-3) / 1e12
+    out = {
+        "metric": "prefill TFLOP/s of one decoder layer at full 8-bit precision",
+        "value": round(value, 1), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms_step, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f16 x, exact integer weights, f32 accumulate",
+        "data": "synthetic (uniform random 8-bit codes and fp16 scales; N(0,1) and SiLU(g)*u activations)",
+        "config": {"workload": "llama3-8b-prefill", "tokens": M,
+                   "layers": {n: [K, N] for n, K, N, _, _ in layers}, "levels": list(levels)},
+        "per_layer": per_layer,
+        "roofline": {"bound": "mfma", "achieved": per_layer[dom]["TFLOPs"], "peak": MFMA_F16_PEAK_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(per_layer[dom]["TFLOPs"] / MFMA_F16_PEAK_TFLOPS, 4),
+                     "traffic": None, "kernel": f"k_prefill ({dom})"},
+        "torch_fp16_dense": {"ms_per_step": round(ms_dense, 4),
+                             "TFLOPs": round(step_flops / (ms_dense * 1e-3) / 1e12, 1)},
+    }
+    if not args.no_cpu:
+        out["cpu_baseline"] = cpu_baseline_prefill(wl, tokens_sample=8)
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse()
     if args.vmm_source_sha:
@@ -323,7 +458,7 @@ def main():
         return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the nested-precision "
-              "VMM path has no multi-GPU mode in this build.", file=sys.stderr)
+              "VMM path runs on a single GPU.", file=sys.stderr)
         sys.exit(2)
     if args.copy_calibration:
         copy_calibration(args.copy_calibration, reps=10)
@@ -334,6 +469,8 @@ def main():
 
     if args.workload == "llama3-8b-decode":
         return run_decode(args, torch, g)
+    if args.workload == "llama3-8b-prefill":
+        return run_prefill(args, torch, g)
 
     dev = torch.device("cuda:0")
     wl = WORKLOADS[args.workload]

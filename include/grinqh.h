@@ -172,6 +172,21 @@ GRINQH_API int grinqh_vmm_threshold(const grinqh_layer_desc* desc, const void* p
                          const float* thresholds, uint8_t* level_map_out, float* y,
                          int32_t flags, void* workspace, size_t ws_bytes, void* stream);
 
+/* Prefill, the stage-decoupled dense path (Sec. 3: prefill reads the weights
+ * at the fixed top precision; Sec. 4 "Prefill vs. Decoding Evaluation"): for
+ * M tokens at once, every channel at all 8 bits,
+ *   Y[m][n] = sum_k X[m][k] * s[k/128][n] * (q[n][k] - 128),
+ * products of fp16 inputs and exact integer weights summed in fp32 per group
+ * of 128 channels, then scaled by the group's fp16 scale in fp32.  Reads the
+ * same packed buffers as grinqh_vmm (any plane_bits and tile_n).
+ *   x: fp16 [M][K] (device, 16-byte aligned), finite; y: fp32 [M][N]
+ *   (device, 4-byte aligned); 1 <= M <= 2^24.
+ *   flags: 0 -> y is overwritten; GRINQH_VMM_ACCUMULATE -> y += result.
+ * The summation order is fixed, so a result is reproducible bit for bit. */
+GRINQH_API int grinqh_prefill(const grinqh_layer_desc* desc, const void* packed_codes,
+                              const void* packed_scales, const void* x, int32_t M, float* y,
+                              int32_t flags, void* stream);
+
 /* Message of the last failing call on this thread ("" if none). */
 GRINQH_API const char* grinqh_last_error(void);
 

@@ -201,6 +201,21 @@ def vmm_batch(codes, scales, x16, levels, level_bits, group: int = 128) -> np.nd
                      for t in range(x16.shape[0])])
 
 
+def prefill(codes, scales, x16, group: int = 128) -> np.ndarray:
+    """Stage-decoupled prefill (Sec. 3: the prompt is processed with the
+    weights at the fixed top precision b_max; Sec. 4 "Prefill vs. Decoding
+    Evaluation": unpack at b_max, dense matrix-matrix product).  Every channel
+    of every token is read at 8 bits, so W_hat = s (q - 128) (R1, R3) and
+    Y = X W_hat^T for the M tokens in x16 [M, K] (float64 [M, N])."""
+    codes = np.asarray(codes)
+    N, K = codes.shape
+    s_full = np.repeat(np.asarray(scales, dtype=np.float16).astype(np.float64).T,
+                       group, axis=1)                          # [N, K]
+    W = reconstruct(codes, s_full, B_MAX)
+    X = np.atleast_2d(np.asarray(x16, dtype=np.float16)).astype(np.float64)
+    return X @ W.T
+
+
 # ---------------------------------------------------------------------------
 # 6. Packed nested layout (Sec. 3.3 and App. C.1, as re-laid-out for CDNA4)
 # ---------------------------------------------------------------------------

@@ -293,6 +293,24 @@ int grinqh_vmm_threshold(const grinqh_layer_desc* desc, const void* packed_codes
                     flags & GRINQH_VMM_ACCUMULATE, (hipStream_t)stream);
 }
 
+int grinqh_prefill(const grinqh_layer_desc* desc, const void* packed_codes,
+                   const void* packed_scales, const void* x, int32_t M, float* y, int32_t flags,
+                   void* stream) {
+  clear_error();
+  Layer L;
+  int st = resolve(desc, &L, nullptr);
+  if (st) return st;
+  if (!packed_codes || !packed_scales || !x || !y)
+    return fail(GRINQH_EINVAL, "codes, scales, x and y must not be NULL");
+  if (M < 1 || M > (1 << 24)) return fail(GRINQH_EINVAL, "M=%d outside 1..2^24", M);
+  if (flags & ~GRINQH_VMM_ACCUMULATE) return fail(GRINQH_EINVAL, "unknown flags 0x%x", flags);
+  if (((uintptr_t)packed_codes | (uintptr_t)packed_scales | (uintptr_t)x) & 15u)
+    return fail(GRINQH_EINVAL, "packed codes, scales and x must be 16-byte aligned");
+  if ((uintptr_t)y & 3u) return fail(GRINQH_EINVAL, "y must be 4-byte aligned");
+  return launch_prefill(L, packed_codes, packed_scales, x, M, y, flags & GRINQH_VMM_ACCUMULATE,
+                        (hipStream_t)stream);
+}
+
 const char* grinqh_last_error(void) { return g_err; }
 
 }  // extern "C"

@@ -83,5 +83,7 @@ int launch_vmm_dot2(const Layer& L, const void* codes, const void* scales, const
 int launch_vmm(const Layer& L, const void* codes, const void* scales, const void* x,
                const uint8_t* level_map, const Thresholds* th, uint8_t* level_map_out,
                int B, float* y, int accumulate, hipStream_t s);
+int launch_prefill(const Layer& L, const void* codes, const void* scales, const void* x, int M,
+                   float* y, int accumulate, hipStream_t s);
 
 }  // namespace grinqh

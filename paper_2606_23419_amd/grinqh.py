@@ -30,7 +30,7 @@ MAX_LEVELS = 9
 EXPORTED = (
     "grinqh_resolve_desc", "grinqh_packed_bytes", "grinqh_pack", "grinqh_topk_counts",
     "grinqh_workspace_bytes", "grinqh_calibrate", "grinqh_assign", "grinqh_vmm",
-    "grinqh_vmm_threshold", "grinqh_last_error",
+    "grinqh_vmm_threshold", "grinqh_prefill", "grinqh_last_error",
 )
 
 
@@ -75,6 +75,7 @@ def _load():
         "grinqh_vmm": [dp, vp, vp, vp, vp, i32, vp, i32, vp, sz, vp],
         "grinqh_vmm_threshold": [dp, vp, vp, vp, i32, ctypes.POINTER(ctypes.c_float), vp, vp,
                                  i32, vp, sz, vp],
+        "grinqh_prefill": [dp, vp, vp, vp, i32, vp, i32, vp],
     }
     for name, args in sig.items():
         f = getattr(lib, name)
@@ -280,4 +281,23 @@ def grinqh_vmm_threshold(desc: LayerDesc, packed_codes, packed_scales, x, thresh
     flags = GRINQH_VMM_ACCUMULATE if accumulate else 0
     _check(lib.grinqh_vmm_threshold(ctypes.byref(rd), cp, sp, xp, B, _floats(thresholds), lo,
                                     yp, flags, None, 0, _stream(stream)))
+    return y
+
+
+def grinqh_prefill(desc: LayerDesc, packed_codes, packed_scales, x, y=None,
+                   accumulate: bool = False, stream=None):
+    """Y fp32 [M, N] = X W_hat^T at all 8 bits for fp16 X [M, K] (prefill)."""
+    torch = _torch()
+    rd = grinqh_resolve_desc(desc)
+    if x.dim() == 1:
+        x = x.view(1, -1)
+    M = int(x.shape[0])
+    cp = _dev(packed_codes, torch.uint8, "packed_codes", (rd.K * rd.N,))
+    sp = _dev(packed_scales, torch.float16, "packed_scales", (rd.K // 128, rd.N))
+    xp = _dev(x, torch.float16, "x", (M, rd.K))
+    if y is None:
+        y = torch.empty((M, rd.N), dtype=torch.float32, device=x.device)
+    yp = _dev(y, torch.float32, "y", (M, rd.N))
+    flags = GRINQH_VMM_ACCUMULATE if accumulate else 0
+    _check(lib.grinqh_prefill(ctypes.byref(rd), cp, sp, xp, M, yp, flags, _stream(stream)))
     return y

@@ -172,6 +172,21 @@ def test_vmm_validation(g):
     assert g.grinqh_last_error()
 
 
+def test_prefill_validation(g):
+    d = g.make_desc(256, 512, (0, 2, 4, 8))
+    P = g.lib.grinqh_prefill
+    assert P(ctypes.byref(d), FAKE, FAKE, FAKE, 0, FAKE, 0, None) == -1
+    assert P(ctypes.byref(d), FAKE, FAKE, FAKE, (1 << 24) + 1, FAKE, 0, None) == -1
+    assert P(ctypes.byref(d), None, FAKE, FAKE, 1, FAKE, 0, None) == -1
+    assert P(ctypes.byref(d), FAKE, FAKE, FAKE, 1, None, 0, None) == -1
+    assert P(ctypes.byref(d), FAKE, FAKE, FAKE, 1, FAKE, 2, None) == -1
+    assert P(ctypes.byref(d), FAKE, FAKE, ctypes.c_void_p(0x1008), 1, FAKE, 0, None) == -1
+    assert "16-byte" in g.grinqh_last_error()
+    assert P(ctypes.byref(d), FAKE, FAKE, FAKE, 1, ctypes.c_void_p(0x1002), 0, None) == -1
+    bad = g.make_desc(200, 512, (0, 8))
+    assert P(ctypes.byref(bad), FAKE, FAKE, FAKE, 1, FAKE, 0, None) == -1
+
+
 def test_binding_rejects_host_tensors(g):
     import torch
     d = g.make_desc(256, 512, (0, 2, 4, 8))

@@ -380,3 +380,97 @@ def test_vmm_groups_with_no_active_channel(g, torch, tile_n, gw, monkeypatch):
     x = inputs.activations_t3(K, 1, 66)
     y, ref = _vmm_case(g, torch, L, x, lm)
     assert normwise(y, ref) <= TOL
+
+
+# --------------------------------------------------------------- prefill ----
+def rowwise(y, ref):
+    """Largest over rows of max_n |y - ref| / max_n |ref|."""
+    y, ref = np.asarray(y, dtype=np.float64), np.asarray(ref, dtype=np.float64)
+    den = np.maximum(np.abs(ref).max(axis=1), 1e-30)
+    return float((np.abs(y - ref).max(axis=1) / den).max())
+
+
+# products of fp16 inputs and integer weights are exact in fp32; only the
+# fp32 sums round, so the kernel sits far inside the 1e-3 bar
+PREFILL_TOL = 1e-5
+
+PREFILL = [  # K, N, levels, tile_n, M
+    (128, 256, (0, 2, 4, 8), 256, 1),
+    (384, 512, (0, 2, 4, 8), 512, 200),
+    (640, 1024, (0, 2, 4, 6, 8), 1024, 130),
+    (1152, 512, (0, 2, 4, 8), 256, 257),
+    (256, 2048, (0, 2, 4, 8), 2048, 64),
+    (256, 2048, (0, 2, 3, 4, 8), 2048, 77),    # 1-bit planes
+    (256, 1024, (0, 2, 3, 4, 8), 512, 300),    # 1-bit planes
+]
+
+
+@pytest.mark.parametrize("K,N,levels,tile_n,M", PREFILL)
+def test_prefill_parity(g, torch, K, N, levels, tile_n, M):
+    L = Layer(g, torch, K, N, levels, cfg=60, layer=K + M, tile_n=tile_n)
+    assert L.desc.plane_bits == (1 if 3 in levels else 2)
+    x = inputs.activations_t3(K, M, 60, K + M)
+    y = _host(g.grinqh_prefill(L.desc, L.pc, L.ps, _dev(torch, x)))
+    ref = orc.prefill(L.codes, L.scales, x)
+    assert normwise(y, ref) <= TOL
+    assert rowwise(y, ref) <= PREFILL_TOL
+
+
+def test_prefill_codes_source_all_code_values(g, torch):
+    # uniform codes reach every byte value, including 0 and 255
+    K, N, M = 512, 1024, 129
+    L = Layer(g, torch, K, N, (0, 2, 4, 8), cfg=61, layer=1, codes_src=True)
+    assert L.codes.min() == 0 and L.codes.max() == 255
+    x = inputs.activations_swiglu(K, M, 61, 1)
+    y = _host(g.grinqh_prefill(L.desc, L.pc, L.ps, _dev(torch, x)))
+    assert rowwise(y, orc.prefill(L.codes, L.scales, x)) <= PREFILL_TOL
+
+
+def test_prefill_accumulate_and_reproducible(g, torch):
+    K, N, M = 384, 512, 150
+    L = Layer(g, torch, K, N, (0, 2, 4, 8), cfg=62, layer=2)
+    x = inputs.activations_t3(K, M, 62, 2)
+    xd = _dev(torch, x)
+    y1 = _host(g.grinqh_prefill(L.desc, L.pc, L.ps, xd))
+    y2 = _host(g.grinqh_prefill(L.desc, L.pc, L.ps, xd))
+    assert np.array_equal(y1.view(np.uint32), y2.view(np.uint32))
+    base = np.random.default_rng(3).standard_normal((M, N)).astype(np.float32)
+    yd = _dev(torch, base)
+    g.grinqh_prefill(L.desc, L.pc, L.ps, xd, y=yd, accumulate=True)
+    ref = orc.prefill(L.codes, L.scales, x) + base.astype(np.float64)
+    assert rowwise(_host(yd), ref) <= PREFILL_TOL
+
+
+def test_prefill_rows_match_decode_at_top_level(g, torch):
+    # the two stages read one packed copy: a prefill row is the decode VMM
+    # with every channel at the top level
+    K, N, M = 1024, 2048, 4
+    levels = (0, 2, 4, 6, 8)
+    L = Layer(g, torch, K, N, levels, cfg=63, layer=3)
+    x = inputs.activations_t3(K, M, 63, 3)
+    xd = _dev(torch, x)
+    y = _host(g.grinqh_prefill(L.desc, L.pc, L.ps, xd))
+    top = _dev(torch, np.full((M, K), len(levels) - 1, dtype=np.uint8))
+    yv = _host(g.grinqh_vmm(L.desc, L.pc, L.ps, xd, top))
+    assert rowwise(y, yv) <= PREFILL_TOL
+
+
+PREFILL_FULL = [  # name, K, N, levels, M
+    ("qkv 4096->6144 M2048", 4096, 6144, inputs.LEVELS_B, 2048),
+    ("gate_up 4096->28672 M512", 4096, 28672, inputs.LEVELS_B, 512),
+    ("down 14336->4096 M300", 14336, 4096, inputs.LEVELS_B, 300),
+]
+
+
+@pytest.mark.parametrize("name,K,N,levels,M", PREFILL_FULL, ids=[f[0] for f in PREFILL_FULL])
+def test_prefill_full_size_sampled(g, torch, name, K, N, levels, M):
+    L = Layer(g, torch, K, N, levels, cfg=71, layer=K + N)
+    gen = inputs.activations_swiglu if K > N else inputs.activations_t3
+    x = gen(K, M, 71, K + N)
+    y = _host(g.grinqh_prefill(L.desc, L.pc, L.ps, _dev(torch, x)))
+    assert np.all(np.isfinite(y))
+    r = np.random.default_rng(K + N)
+    rows = np.sort(r.choice(M, size=min(M, 48), replace=False))
+    cols = np.sort(r.choice(N, size=256, replace=False))
+    ref = orc.prefill(L.codes[cols], L.scales[:, cols], x[rows])
+    assert rowwise(y[np.ix_(rows, cols)], ref) <= PREFILL_TOL, name

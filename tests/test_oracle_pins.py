@@ -156,6 +156,48 @@ def test_vmm_all_top_is_textbook_dequant_matvec():
     assert np.max(np.abs(y - dense)) < 0.02 * np.max(np.abs(dense)) + 1e-3
 
 
+def test_prefill_bruteforce_exact():
+    # every channel at 8 bits, each token's row summed exactly in rationals
+    G, N, K, M = 128, 5, 256, 3
+    codes = inputs.random_codes(N, K, 3, 1)
+    scales = inputs.random_scales(N, K, G, 3, 1).T.copy()          # [K/G, N]
+    x = inputs.activations_t3(K, M, 3, 1)
+    got = orc.prefill(codes, scales, x)
+    cq = codes.astype(int).tolist()
+    sc_f = [[Fraction(float(scales[g, n])) for n in range(N)] for g in range(K // G)]
+    for m in range(M):
+        x_f = [Fraction(float(v)) for v in x[m]]
+        want = bf.vmm_exact(cq, sc_f, x_f, [1] * K, (0, 8), G)
+        np.testing.assert_allclose(got[m], [float(v) for v in want], rtol=1e-12, atol=0)
+
+
+def test_prefill_unit_tokens_read_single_weights():
+    # token m = 2^-3 e_k reads back 2^-3 s[k // 128][n] (q[n][k] - 128) exactly:
+    # a transposed operand, a wrong group index or a dropped offset all fail
+    G, N, K = 128, 6, 384
+    codes = inputs.random_codes(N, K, 4, 2)
+    scales = inputs.random_scales(N, K, G, 4, 2).T.copy()
+    ks = [0, 1, 127, 128, 200, 383]
+    x = np.zeros((len(ks), K), dtype=np.float16)
+    for m, k in enumerate(ks):
+        x[m, k] = 0.125
+    y = orc.prefill(codes, scales, x)
+    for m, k in enumerate(ks):
+        for n in range(N):
+            assert y[m, n] == 0.125 * float(scales[k // G, n]) * (int(codes[n, k]) - 128)
+
+
+def test_prefill_rows_equal_decode_at_top_level():
+    G, N, K, M = 128, 16, 512, 4
+    codes = inputs.random_codes(N, K, 5, 3)
+    scales = inputs.random_scales(N, K, G, 5, 3).T.copy()
+    x = inputs.activations_t3(K, M, 5, 3)
+    top = np.full((M, K), 3, dtype=np.uint8)
+    np.testing.assert_allclose(orc.prefill(codes, scales, x),
+                               orc.vmm_batch(codes, scales, x, top, (0, 2, 4, 8)),
+                               rtol=1e-13, atol=1e-13)
+
+
 def test_vmm_all_skipped_is_zero():
     W = inputs.weights(32, 256, config=97)
     x = inputs.activations_t3(256, 1, config=97)[0]
