@@ -78,20 +78,28 @@ WORKLOADS = {
 MFMA_F16_PEAK_TFLOPS = 2500.0
 
 
+PREFILL_SOURCES = ("paper_2606_23419_amd/csrc/prefill.hip", "paper_2606_23419_amd/csrc/grinqh_internal.h")
+
+
 def vmm_source_sha() -> str:
+    return source_sha(VMM_SOURCES)
+
+
+def source_sha(sources) -> str:
     import hashlib
     h = hashlib.sha256()
-    for rel in VMM_SOURCES:
+    for rel in sources:
         with open(os.path.join(ROOT, rel), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
 
 
-def stored_traffic(workload: str, budget: int, assign: str):
-    """HBM bytes per VMM launch from the committed rocprofv3 FETCH_SIZE /
-    WRITE_SIZE summary of this workload, or None when there is none or the
-    kernel sources changed since it was taken."""
-    path = os.path.join(PROFILES, f"k_vmm_traffic_{workload}_{assign}_b{budget}.md")
+def stored_traffic(workload: str, budget: int, assign: str, path=None, sources=VMM_SOURCES):
+    """HBM bytes per launch from a committed rocprofv3 FETCH_SIZE / WRITE_SIZE
+    summary (by default the VMM kernel's on this workload), or None when there
+    is none or the kernel sources changed since it was taken."""
+    if path is None:
+        path = os.path.join(PROFILES, f"k_vmm_traffic_{workload}_{assign}_b{budget}.md")
     if not os.path.exists(path):
         return None
     fields = {}
@@ -100,7 +108,7 @@ def stored_traffic(workload: str, budget: int, assign: str):
             if ":" in line and not line.startswith(("#", "|", " ")):
                 k, v = line.split(":", 1)
                 fields[k.strip()] = v.strip()
-    if fields.get("source_sha256_16") != vmm_source_sha():
+    if fields.get("source_sha256_16") != source_sha(sources):
         return None
     try:
         return float(fields["traffic_bytes_per_launch"])
@@ -134,6 +142,7 @@ def parse():
     ap.add_argument("--batch", type=int, default=1, help="tokens per VMM call (decode workload)")
     ap.add_argument("--n-layers", type=int, default=0, help="decoder layers (decode workload)")
     ap.add_argument("--prefill-tokens", type=int, default=0, help="prompt tokens M (prefill workload)")
+    ap.add_argument("--layer", default=None, help="prefill workload: run only this projection")
     ap.add_argument("--tile-n", type=int, default=0)
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
     ap.add_argument("--vmm-only-reps", type=int, default=5)
@@ -356,6 +365,11 @@ def run_prefill(args, torch, g):
     dev = torch.device("cuda:0")
     wl = WORKLOADS["llama3-8b-prefill"]
     levels, layers = wl["levels"], wl["layers"]
+    if args.layer:
+        layers = [l for l in layers if l[0] == args.layer]
+        if not layers:
+            print(f"--layer must be one of {[l[0] for l in wl['layers']]}", file=sys.stderr)
+            sys.exit(2)
     M = args.prefill_tokens or wl["tokens"]
     gen = torch.Generator(device=dev)
     gen.manual_seed(6)
@@ -435,19 +449,22 @@ def run_prefill(args, torch, g):
         "metric": "prefill TFLOP/s of one decoder layer at full 8-bit precision",
         "value": round(value, 1), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(ms_step, 4), "higher_is_better": True,
-        "scaling": "weak", "vs_baseline": None, "dtype": "f16 x, exact integer weights, f32 accumulate",
+        "scaling": "weak", "vs_baseline": None, "dtype": "f16 x, f16 dequantised weights, f32 accumulate",
         "data": "synthetic (uniform random 8-bit codes and fp16 scales; N(0,1) and SiLU(g)*u activations)",
         "config": {"workload": "llama3-8b-prefill", "tokens": M,
                    "layers": {n: [K, N] for n, K, N, _, _ in layers}, "levels": list(levels)},
         "per_layer": per_layer,
         "roofline": {"bound": "mfma", "achieved": per_layer[dom]["TFLOPs"], "peak": MFMA_F16_PEAK_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(per_layer[dom]["TFLOPs"] / MFMA_F16_PEAK_TFLOPS, 4),
-                     "traffic": None, "kernel": f"k_prefill ({dom})"},
+                     "traffic": stored_traffic(None, None, None, sources=PREFILL_SOURCES,
+                                               path=os.path.join(PROFILES, f"k_prefill_traffic_llama3-8b-prefill_{dom}.md"))
+                     if M == wl["tokens"] else None,
+                     "kernel": f"k_prefill ({dom})"},
         "torch_fp16_dense": {"ms_per_step": round(ms_dense, 4),
                              "TFLOPs": round(step_flops / (ms_dense * 1e-3) / 1e12, 1)},
     }
     if not args.no_cpu:
-        out["cpu_baseline"] = cpu_baseline_prefill(wl, tokens_sample=8)
+        out["cpu_baseline"] = cpu_baseline_prefill(wl, tokens_sample=256)
     print(json.dumps(out), flush=True)
 
 

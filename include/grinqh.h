@@ -175,9 +175,10 @@ GRINQH_API int grinqh_vmm_threshold(const grinqh_layer_desc* desc, const void* p
 /* Prefill, the stage-decoupled dense path (Sec. 3: prefill reads the weights
  * at the fixed top precision; Sec. 4 "Prefill vs. Decoding Evaluation"): for
  * M tokens at once, every channel at all 8 bits,
- *   Y[m][n] = sum_k X[m][k] * s[k/128][n] * (q[n][k] - 128),
- * products of fp16 inputs and exact integer weights summed in fp32 per group
- * of 128 channels, then scaled by the group's fp16 scale in fp32.  Reads the
+ *   Y[m][n] = sum_k X[m][k] * w_hat[n][k],  w_hat = s[k/128][n] * (q[n][k] - 128),
+ * with each w_hat rounded once to fp16 (the dequantised weight of a dense
+ * fp16 GEMM), fp16 x fp16 products and fp32 accumulation: per element
+ * |Y - exact| <= (2^-11 + K 2^-24) sum_k |X[m][k]| |w_hat[n][k]|.  Reads the
  * same packed buffers as grinqh_vmm (any plane_bits and tile_n).
  *   x: fp16 [M][K] (device, 16-byte aligned), finite; y: fp32 [M][N]
  *   (device, 4-byte aligned); 1 <= M <= 2^24.

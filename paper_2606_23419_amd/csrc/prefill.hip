@@ -1,26 +1,29 @@
 // Prefill over the nested layout: the stage-decoupled path of Sec. 3 (prefill
 // reads the weights at the fixed top precision b_max and multiplies densely;
 // Sec. 4 "Prefill vs. Decoding Evaluation").  For M tokens at once,
-//   Y[m][n] = sum_g s[g][n] * sum_{k in g} X[m][k] (q[n][k] - 128),
+//   Y[m][n] = sum_k X[m][k] W_hat[n][k],  W_hat = s[k/128][n] (q[n][k] - 128),
 // a dense contraction, on the matrix cores (v_mfma_f32_32x32x16_f16).
 //
-// A workgroup of 4 waves computes a 128 x 128 tile of Y; wave w owns the
-// 64 x 64 sub-tile (w / 2, w % 2) as 2 x 2 MFMA blocks of 32 x 32.  K runs
-// one quantisation group of 128 channels at a time:
-//   - the X tile [128 m][128 k] is copied to LDS, k contiguous;
-//   - the codes of the tile's 128 outputs and the group's 128 channels are
-//     read from the bit planes (one dword of 16 outputs per channel and
-//     2-bit plane, or one 16-bit word per 1-bit plane), assembled into bytes,
-//     turned into the fp16 values q - 128 (exact: 0x6400 | q reads as
-//     1024 + q), and written to LDS transposed, [n][k], so that each MFMA
-//     operand fragment (eight consecutive k of one m or one n) is a single
-//     16-byte LDS read;
-//   - 8 MFMA steps of k = 16 accumulate the group's integer-weight product
-//     in fp32, and s[g][n] scales it into the output sums.
-// LDS rows are 256 bytes with the 16-byte chunks XOR-swizzled per row, which
-// keeps both the transposed writes and the fragment reads free of bank
-// conflicts beyond their minimum.  The next group's global loads are issued
-// before the current group's MFMAs.
+// A workgroup of 4 waves computes a (64 MB) x (64 NB) tile of Y; each wave
+// owns a (32 MB) x (32 NB) quarter as MB x NB blocks of 32 x 32, so every
+// 16-byte operand fragment read from LDS feeds NB (or MB) MFMAs.  K advances
+// 64 channels per step through two LDS buffers: while the waves multiply out
+// of one buffer they fill the other with the next step,
+//   - X: the [64 MB rows][64 k] fp16 tile, copied;
+//   - W: the codes of the tile's 64 NB outputs for 64 channels, read from the
+//     bit planes (one dword of 16 outputs per channel and 2-bit plane, or a
+//     16-bit word per 1-bit plane), assembled into bytes, turned into fp16
+//     q - 128 (exact: 0x6400 | q reads as 1024 + q), multiplied by the fp16
+//     group scale (one rounding: the dequantised weight in fp16, as a dense
+//     GEMM over unpacked weights uses it), and written transposed, [n][k],
+//     so that an MFMA fragment (eight consecutive k of one row) is one
+//     16-byte LDS read.
+// Global loads for step s + 2 are issued while step s is multiplied.  LDS
+// rows are 128 bytes with XOR-swizzled 16-byte chunks, so fragment reads and
+// the tile copies are free of bank conflicts and the transposed weight
+// writes are at most 2-way.
+#include <cstdlib>
+
 #include "grinqh_internal.h"
 
 namespace grinqh {
@@ -31,12 +34,19 @@ typedef _Float16 half8 __attribute__((ext_vector_type(8)));
 typedef _Float16 half2v __attribute__((ext_vector_type(2)));
 typedef float float16v __attribute__((ext_vector_type(16)));
 
-constexpr int kBM = 128, kBN = 128, kBK = 128;
+constexpr int kBK = 64;
 constexpr int kThreadsPF = 256;
 
-// fp16 pair (q_a - 128, q_b - 128) from code bytes at bits 0..7 and 16..23.
-__device__ __forceinline__ uint32_t codes_to_half2(uint32_t v) {
-  const half2v h = __builtin_bit_cast(half2v, v | 0x64006400u);
+__device__ __forceinline__ uint32_t mul_half2(uint32_t a, uint32_t b) {
+  return __builtin_bit_cast(uint32_t, __builtin_bit_cast(half2v, a) * __builtin_bit_cast(half2v, b));
+}
+
+// fp16 pair (q_a - 128, q_b - 128) from bytes a and b (selector byte
+// indices 0..3) of the code word q: one v_perm_b32 places each code under
+// an exponent byte 0x64, so a half reads 1024 + q exactly.
+__device__ __forceinline__ uint32_t codes_to_half2(uint32_t q, uint32_t a, uint32_t b) {
+  const uint32_t v = __builtin_amdgcn_perm(0x64646464u, q, a | 0x0400u | (b << 16) | 0x04000000u);
+  const half2v h = __builtin_bit_cast(half2v, v);
   const half2v c = {(_Float16)1152.0f, (_Float16)1152.0f};
   return __builtin_bit_cast(uint32_t, h - c);
 }
@@ -66,165 +76,280 @@ __device__ __forceinline__ void assemble_codes(uint32_t w1, uint32_t w2, uint32_
   q[3] = (O12 & 0xF0F0F0F0u) | ((O34 >> 4) & 0x0F0F0F0Fu);
 }
 
-// LDS element offsets (in halves) of 16-byte chunk c of row r.
-__device__ __forceinline__ int x_chunk(int m, int c) { return m * kBK + 8 * (c ^ (m & 15)); }
-__device__ __forceinline__ int w_chunk(int n, int c) {
-  return n * kBK + 8 * (c ^ ((n & 15) ^ ((n >> 2) & 12)));
+// LDS offsets (halves) of 16-byte chunk c of a 64-half row.  The swizzles
+// make eight (or sixteen) consecutive rows at one chunk hit distinct banks;
+// for weight rows bit 4 of the row also moves the chunk by 4, so that the
+// transposed writes of one instruction (8 channel quads of two rows 16
+// apart) fill 128 distinct bytes.  Both depend on the row's low 5 bits only:
+// rows 32 apart differ by a constant offset.
+__device__ __forceinline__ int x_off(int m, int c) {
+  return m * kBK + 8 * (c ^ (m & 7) ^ ((m >> 3) & 1));
+}
+__device__ __forceinline__ int w_off(int n, int c) {
+  return n * kBK + 8 * (c ^ (n & 7) ^ ((n >> 3) & 1) ^ ((n >> 2) & 4));
 }
 
-template <int U>
-__global__ __launch_bounds__(kThreadsPF, 2) void k_prefill(const uint8_t* __restrict__ codes,
+// One step's codes for one thread (CPT channels x 16 outputs as plane
+// words) and the 16 outputs' fp16 scales of the step's group.
+template <int U, int CPT>
+struct WRegs {
+  uint32_t w[CPT][8 / U];
+  uint4 s[2];
+};
+
+template <int U, int MB, int NB>
+__global__ __launch_bounds__(kThreadsPF) void k_prefill(const uint8_t* __restrict__ codes,
                                                        const uint16_t* __restrict__ scales,
                                                        const uint16_t* __restrict__ x,
                                                        float* __restrict__ y, Layer L, int M,
                                                        int accumulate) {
-  constexpr int kWords = 8 / U;   // plane words per channel row and 16 outputs
-  __shared__ __align__(16) _Float16 sX[kBM * kBK];
-  __shared__ __align__(16) _Float16 sW[kBN * kBK];
+  constexpr int BM = 64 * MB, BN = 64 * NB;
+  constexpr int XI = BM * kBK * 2 / 1024 / 4;      // X copy instructions per wave and step
+  constexpr int WI = kBK * BN / 1024 / 4;          // code copy instructions per wave and step
+  constexpr int RCH = BN / 16;                     // 16-byte chunks of one staged channel row
+  constexpr int PPP = BN * U / 128;                // chunks per plane of a staged row
+  constexpr int CPT = BN / 64;                     // channels per thread and step
+  constexpr int NCG = kBK / CPT;                   // channel groups per step
+  constexpr int kWords = 8 / U;                    // plane words per channel and 16 outputs
+  static_assert(CPT == 2 || CPT == 4, "tile width");
+  // separate objects per buffer: the compiler then knows that a copy in
+  // flight into one buffer does not alias reads of the other
+  __shared__ __align__(16) _Float16 sX0[BM * kBK];
+  __shared__ __align__(16) _Float16 sX1[BM * kBK];
+  __shared__ __align__(16) _Float16 sW0[BN * kBK];
+  __shared__ __align__(16) _Float16 sW1[BN * kBK];
+  __shared__ __align__(16) uint8_t sP0[kBK * BN];  // raw codes of a step (BN bytes per channel)
+  __shared__ __align__(16) uint8_t sP1[kBK * BN];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int m0 = blockIdx.x * kBM, n0 = blockIdx.y * kBN;
+  const int m0 = blockIdx.x * BM, n0 = blockIdx.y * BN;
   const int T = L.T, K = L.K, N = L.N;
-  const int tile = n0 / T, o0 = n0 - tile * T;   // 128 divides T
-  const int wm = (wave >> 1) * 64, wn = (wave & 1) * 64;
+  const int steps = K / kBK;                       // even: K is a multiple of 128
+  const int tile = n0 / T, o0 = n0 - tile * T;     // BN divides T
+  const int wm = (wave >> 1) * 32 * MB, wn = (wave & 1) * 32 * NB;
 
-  // X copy: 16-byte chunk xc of rows 16 i + xq (rows past M repeat row M-1;
-  // their outputs are never stored)
-  const int xq = tid >> 4, xc = tid & 15;
-  // W unpack: channels wr..wr+3 of the group, outputs wc..wc+15 of the tile
-  const int wr = 4 * ((lane & 7) + 8 * wave), wc = 16 * (lane >> 3);
-  const int plane_bytes = T * U / 8;
-  const uint8_t* wbase = codes + ((size_t)tile * K + wr) * T + (o0 + wc) * U / 8;
-  const uint16_t* sbase = scales + n0 + wn + (lane & 31);
-
-  uint4 xv[8];
-  uint32_t wv[4][kWords];
-  uint16_t sv[2];
-  auto load_group = [&](int g) {
+  // X copy: instruction i of this wave fills LDS rows 8 I .. 8 I + 7, I = 4 i +
+  // wave, 16 bytes per lane; lane l takes the logical chunk that the swizzle
+  // puts at physical chunk l % 8 of row 8 I + l / 8.  Rows past M repeat row
+  // M - 1 (never stored).
+  const uint16_t* xsrc[XI];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int m = min(m0 + 16 * i + xq, M - 1);
-      xv[i] = *(const uint4*)(x + (size_t)m * K + g * kBK + 8 * xc);
-    }
+  for (int i = 0; i < XI; ++i) {
+    const int row = 8 * (4 * i + wave) + (lane >> 3);
+    const int c = (lane & 7) ^ (row & 7) ^ ((row >> 3) & 1);
+    xsrc[i] = x + (size_t)min(m0 + row, M - 1) * K + 8 * c;
+  }
+  auto copy_x = [&](int st, _Float16* sx) __attribute__((always_inline)) {
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const uint8_t* row = wbase + (size_t)(g * kBK + r) * T;
-#pragma unroll
-      for (int j = 0; j < kWords; ++j) {
-        if constexpr (U == 2)
-          wv[r][j] = *(const uint32_t*)(row + j * plane_bytes);
-        else
-          wv[r][j] = *(const uint16_t*)(row + j * plane_bytes);
-      }
-    }
-    sv[0] = sbase[(size_t)g * N];
-    sv[1] = sbase[(size_t)g * N + 32];
+    for (int i = 0; i < XI; ++i)
+      __builtin_amdgcn_global_load_lds(
+          (const __attribute__((address_space(1))) void*)(xsrc[i] + st * kBK),
+          (__attribute__((address_space(3))) void*)&sx[8 * kBK * (4 * i + wave)], 16, 0, 0);
   };
-  auto store_group = [&]() {
+
+  // Code staging: the tile's part of a channel row is BN bytes (every plane's
+  // BN u / 8 bytes).  Staged chunk slot v of row r (v = plane * PPP + piece)
+  // sits at position v ^ ((r / CPT) & 7) of the row, so the word reads below
+  // (8 channel groups x 8 output chunks per instruction) hit distinct banks.
+  const uint8_t* wtile = codes + (size_t)tile * K * T + o0 * U / 8;
+  int wsrc[WI];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) *(uint4*)&sX[x_chunk(16 * i + xq, xc)] = xv[i];
-    // h[r][d][p]: fp16 values of outputs 8p + d (low half) and 8p + 4 + d
-    // (high half) of channel wr + r
-    uint32_t h[4][4][2];
+  for (int i = 0; i < WI; ++i) {
+    const int q = 64 * (4 * i + wave) + lane;
+    const int r = q / RCH, v = (q % RCH) ^ ((r / CPT) & 7);
+    wsrc[i] = r * T + (v / PPP) * (T * U / 8) + 16 * (v % PPP);
+  }
+  auto copy_w = [&](int st, uint8_t* sp) __attribute__((always_inline)) {
+    const uint8_t* base = wtile + (size_t)st * kBK * T;
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      uint32_t w[4];
-      if constexpr (U == 2) {
+    for (int i = 0; i < WI; ++i)
+      __builtin_amdgcn_global_load_lds(
+          (const __attribute__((address_space(1))) void*)(base + wsrc[i]),
+          (__attribute__((address_space(3))) void*)&sp[1024 * (4 * i + wave)], 16, 0, 0);
+  };
+
+  // W unpack: outputs 16 j .. 16 j + 15 of the tile, channels CPT cg .. of the step
+  const int cg = (lane & 7) + 8 * (wave % (NCG / 8));
+  const int j = (lane >> 3) + 8 * (wave / (NCG / 8));
+  const uint16_t* sbase = scales + n0 + 16 * j;
+  auto load_scales = [&](int st, WRegs<U, CPT>& R) __attribute__((always_inline)) {
+    const uint4* sg = (const uint4*)(sbase + (size_t)(st * kBK / kGroup) * N);
+    R.s[0] = sg[0];
+    R.s[1] = sg[1];
+  };
+  auto read_w = [&](const uint8_t* sp, WRegs<U, CPT>& R) __attribute__((always_inline)) {
 #pragma unroll
-        for (int j = 0; j < 4; ++j) w[j] = wv[r][j];
-      } else {
+    for (int r = 0; r < CPT; ++r) {
+      const int row = cg * CPT + r;
 #pragma unroll
-        for (int j = 0; j < 4; ++j) w[j] = (spread_bits(wv[r][2 * j]) << 1) | spread_bits(wv[r][2 * j + 1]);
-      }
-      uint32_t q[4];
-      assemble_codes(w[0], w[1], w[2], w[3], q);
-#pragma unroll
-      for (int d = 0; d < 4; ++d) {
-        h[r][d][0] = codes_to_half2(__builtin_amdgcn_perm(0u, q[d], 0x0C010C00u));
-        h[r][d][1] = codes_to_half2(__builtin_amdgcn_perm(0u, q[d], 0x0C030C02u));
+      for (int p = 0; p < kWords; ++p) {
+        if constexpr (U == 2) {
+          const int v = (p * PPP + (j >> 2)) ^ (cg & 7);
+          R.w[r][p] = *(const uint32_t*)&sp[16 * (row * RCH + v) + 4 * (j & 3)];
+        } else {
+          const int v = (p * PPP + (j >> 3)) ^ (cg & 7);
+          R.w[r][p] = *(const uint16_t*)&sp[16 * (row * RCH + v) + 2 * (j & 7)];
+        }
       }
     }
-    // output wc + 4i + d: its four channels' values, k contiguous
+  };
+  // h[r][d][p]: fp16 weights of outputs 8p + d (low half) and 8p + 4 + d
+  // (high half) of channel r
+  auto unpack = [&](const WRegs<U, CPT>& R, int r, uint32_t (&h)[4][2]) __attribute__((always_inline)) {
+    const uint32_t sw[8] = {R.s[0].x, R.s[0].y, R.s[0].z, R.s[0].w,
+                            R.s[1].x, R.s[1].y, R.s[1].z, R.s[1].w};
+    uint32_t w[4];
+    if constexpr (U == 2) {
+#pragma unroll
+      for (int p = 0; p < 4; ++p) w[p] = R.w[r][p];
+    } else {
+#pragma unroll
+      for (int p = 0; p < 4; ++p) w[p] = (spread_bits(R.w[r][2 * p]) << 1) | spread_bits(R.w[r][2 * p + 1]);
+    }
+    uint32_t q[4];
+    assemble_codes(w[0], w[1], w[2], w[3], q);
+#pragma unroll
+    for (int d = 0; d < 4; ++d)
+#pragma unroll
+      for (int p = 0; p < 2; ++p) {
+        // scale pair (s_{8p+d}, s_{8p+4+d})
+        const uint32_t sp = __builtin_amdgcn_perm(sw[4 * p + 2 + (d >> 1)], sw[4 * p + (d >> 1)],
+                                                  (d & 1) ? 0x07060302u : 0x05040100u);
+        h[d][p] = mul_half2(codes_to_half2(q[d], 2 * p, 2 * p + 1), sp);
+      }
+  };
+  const int kq = cg * CPT;
+  // output 16 j + 4 i + d gets the thread's CPT channels, k contiguous
+  auto write_w = [&](_Float16* sw, const uint32_t (&h)[CPT][4][2]) __attribute__((always_inline)) {
 #pragma unroll
     for (int d = 0; d < 4; ++d)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int p = i >> 1;
         const uint32_t sel = (i & 1) ? 0x07060302u : 0x05040100u;
+        _Float16* dst = &sw[w_off(16 * j + 4 * i + d, kq >> 3) + (kq & 7)];
         const uint32_t lo = __builtin_amdgcn_perm(h[1][d][p], h[0][d][p], sel);
-        const uint32_t hi = __builtin_amdgcn_perm(h[3][d][p], h[2][d][p], sel);
-        *(uint2*)&sW[w_chunk(wc + 4 * i + d, wr >> 3) + (wr & 7)] = make_uint2(lo, hi);
+        if constexpr (CPT == 4)
+          *(uint2*)dst = make_uint2(lo, __builtin_amdgcn_perm(h[3][d][p], h[2][d][p], sel));
+        else
+          *(uint32_t*)dst = lo;
       }
   };
 
-  float16v acc[2][2], part[2][2];
+  float16v acc[MB][NB];
 #pragma unroll
-  for (int a = 0; a < 2; ++a)
+  for (int a = 0; a < MB; ++a)
 #pragma unroll
-    for (int b = 0; b < 2; ++b) acc[a][b] = float16v{};
+    for (int b = 0; b < NB; ++b) acc[a][b] = float16v{};
 
-  const int groups = L.groups;
-  load_group(0);
-  for (int g = 0; g < groups; ++g) {
-    const float s0 = h2f(sv[0]), s1 = h2f(sv[1]);
-    __syncthreads();   // every wave has read the previous group's fragments
-    store_group();
-    __syncthreads();
-    if (g + 1 < groups) load_group(g + 1);
-#pragma unroll
-    for (int a = 0; a < 2; ++a)
-#pragma unroll
-      for (int b = 0; b < 2; ++b) part[a][b] = float16v{};
+  // One step st: start the copies of X for st + 1 and of the codes for st + 2
+  // (into the staging buffer that held st's codes) and the scale loads for
+  // st + 2; multiply st out of (xc, wc) while unpacking st + 1 (staged in
+  // pc, scales in `cur`) into (xn, wn_).  Past the last step the copies and
+  // loads re-read the last step (in bounds, never used).
+  auto step = [&](int st, const _Float16* xc, const _Float16* wc, _Float16* xn, _Float16* wn_,
+                  const uint8_t* pc, uint8_t* pn, WRegs<U, CPT>& cur, WRegs<U, CPT>& nxt)
+                  __attribute__((always_inline)) {
+    copy_x(min(st + 1, steps - 1), xn);
+    copy_w(min(st + 2, steps - 1), pn);
+    load_scales(min(st + 2, steps - 1), nxt);
+    __builtin_amdgcn_sched_barrier(0);   // issue them first: a full step of latency
+    read_w(pc, cur);
+    uint32_t h[CPT][4][2];
 #pragma unroll
     for (int ks = 0; ks < kBK / 16; ++ks) {
+      if (ks % (4 / CPT) == 0) unpack(cur, ks / (4 / CPT), h[ks / (4 / CPT)]);
       const int c = 2 * ks + (lane >> 5);
-      half8 fa[2], fb[2];
+      half8 fa[MB], fb[NB];
 #pragma unroll
-      for (int a = 0; a < 2; ++a) fa[a] = *(const half8*)&sX[x_chunk(wm + 32 * a + (lane & 31), c)];
+      for (int a = 0; a < MB; ++a) fa[a] = *(const half8*)&xc[x_off(wm + 32 * a + (lane & 31), c)];
 #pragma unroll
-      for (int b = 0; b < 2; ++b) fb[b] = *(const half8*)&sW[w_chunk(wn + 32 * b + (lane & 31), c)];
+      for (int b = 0; b < NB; ++b) fb[b] = *(const half8*)&wc[w_off(wn + 32 * b + (lane & 31), c)];
 #pragma unroll
-      for (int a = 0; a < 2; ++a)
+      for (int a = 0; a < MB; ++a)
 #pragma unroll
-        for (int b = 0; b < 2; ++b)
-          part[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_f16(fa[a], fb[b], part[a][b], 0, 0, 0);
+        for (int b = 0; b < NB; ++b)
+          acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_f16(fa[a], fb[b], acc[a][b], 0, 0, 0);
+      // one sub-step per scheduling region: the unpack spreads over the MFMAs
+      if (ks + 1 < kBK / 16) __builtin_amdgcn_sched_barrier(0);
     }
+    write_w(wn_, h);
+    __syncthreads();   // copies and writes for st + 1 done; st's reads done
+  };
+
+  WRegs<U, CPT> ra, rb;
+  // prologue: step 0 into buffers 0, codes of step 1 staged in sP1
+  copy_x(0, sX0);
+  copy_w(0, sP0);
+  copy_w(min(1, steps - 1), sP1);
+  load_scales(0, ra);
+  load_scales(min(1, steps - 1), rb);
+  // consume the scale loads before the barrier: left in flight into the loop
+  // they would make the compiler wait for them in every iteration
+  asm volatile("" ::"v"(rb.s[0].x), "v"(rb.s[0].y), "v"(rb.s[0].z), "v"(rb.s[0].w),
+               "v"(rb.s[1].x), "v"(rb.s[1].y), "v"(rb.s[1].z), "v"(rb.s[1].w));
+  __syncthreads();
+  read_w(sP0, ra);
+  {
+    uint32_t h[CPT][4][2];
 #pragma unroll
-    for (int a = 0; a < 2; ++a)
-#pragma unroll
-      for (int j = 0; j < 16; ++j) {
-        acc[a][0][j] = fmaf(s0, part[a][0][j], acc[a][0][j]);
-        acc[a][1][j] = fmaf(s1, part[a][1][j], acc[a][1][j]);
-      }
+    for (int r = 0; r < CPT; ++r) unpack(ra, r, h[r]);
+    write_w(sW0, h);
+  }
+  __syncthreads();   // sP0 is free for the codes of step 2
+  for (int st = 0; st < steps; st += 2) {
+    step(st, sX0, sW0, sX1, sW1, sP1, sP0, rb, ra);
+    step(st + 1, sX1, sW1, sX0, sW0, sP0, sP1, ra, rb);
   }
 
-  // element j of lane l of a 32 x 32 block: row 8 (j / 4) + 4 (l / 32) + j % 4,
+  // element e of lane l of a 32 x 32 block: row 8 (e / 4) + 4 (l / 32) + e % 4,
   // column l % 32
 #pragma unroll
-  for (int a = 0; a < 2; ++a)
+  for (int a = 0; a < MB; ++a)
 #pragma unroll
-    for (int j = 0; j < 16; ++j) {
-      const int m = m0 + wm + 32 * a + 8 * (j >> 2) + 4 * (lane >> 5) + (j & 3);
+    for (int e = 0; e < 16; ++e) {
+      const int m = m0 + wm + 32 * a + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
       if (m >= M) continue;
 #pragma unroll
-      for (int b = 0; b < 2; ++b) {
+      for (int b = 0; b < NB; ++b) {
         float* dst = y + (size_t)m * N + n0 + wn + 32 * b + (lane & 31);
-        *dst = accumulate ? *dst + acc[a][b][j] : acc[a][b][j];
+        *dst = accumulate ? *dst + acc[a][b][e] : acc[a][b][e];
       }
     }
 }
 
+template <int U, int MB, int NB>
+void launch_cfg(const Layer& L, const void* codes, const void* scales, const void* x, int M,
+                float* y, int accumulate, hipStream_t s) {
+  const dim3 grid((unsigned)((M + 64 * MB - 1) / (64 * MB)), (unsigned)(L.N / (64 * NB)));
+  hipLaunchKernelGGL((k_prefill<U, MB, NB>), grid, dim3(kThreadsPF), 0, s, (const uint8_t*)codes,
+                     (const uint16_t*)scales, (const uint16_t*)x, y, L, M, accumulate);
+}
+
+template <int U>
+void launch_u(int cfg, const Layer& L, const void* codes, const void* scales, const void* x, int M,
+              float* y, int accumulate, hipStream_t s) {
+  if (cfg == 0) launch_cfg<U, 4, 4>(L, codes, scales, x, M, y, accumulate, s);
+  else if (cfg == 1) launch_cfg<U, 4, 2>(L, codes, scales, x, M, y, accumulate, s);
+  else launch_cfg<U, 2, 2>(L, codes, scales, x, M, y, accumulate, s);
+}
+
 }  // namespace
 
+// Tile choice: 256 x 256 while that gives at least ~0.6 workgroups per CU
+// (one resident per CU), else 256 x 128 on the same condition, else 128 x 128
+// (short prompts; two resident per CU).  GRINQH_PREFILL_TILE = 0 (256 x 256),
+// 1 (256 x 128) or 2 (128 x 128) forces one.
 int launch_prefill(const Layer& L, const void* codes, const void* scales, const void* x, int M,
                    float* y, int accumulate, hipStream_t s) {
-  const dim3 grid((unsigned)((M + kBM - 1) / kBM), (unsigned)(L.N / kBN));
-  if (L.u == 2)
-    hipLaunchKernelGGL(k_prefill<2>, grid, dim3(kThreadsPF), 0, s, (const uint8_t*)codes,
-                       (const uint16_t*)scales, (const uint16_t*)x, y, L, M, accumulate);
-  else
-    hipLaunchKernelGGL(k_prefill<1>, grid, dim3(kThreadsPF), 0, s, (const uint8_t*)codes,
-                       (const uint16_t*)scales, (const uint16_t*)x, y, L, M, accumulate);
+  const long mb256 = (M + 255) / 256;
+  int cfg = mb256 * (L.N / 256) >= 160 ? 0 : mb256 * (L.N / 128) >= 160 ? 1 : 2;
+  if (const char* e = getenv("GRINQH_PREFILL_TILE")) {
+    const int v = atoi(e);
+    if (v >= 0 && v <= 2) cfg = v;
+  }
+  if (L.u == 2) launch_u<2>(cfg, L, codes, scales, x, M, y, accumulate, s);
+  else launch_u<1>(cfg, L, codes, scales, x, M, y, accumulate, s);
   return check_launch("prefill");
 }
 
