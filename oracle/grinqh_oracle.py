@@ -43,66 +43,73 @@ Readings taken where the paper is silent or inconsistent:
       u = 2; the odd level set {0,2,3,4,8} needs u = 1).
 * R10 phi is the paper's 2^(b_max - b - 1), half a b-bit bin above the floor,
       not the exact centre of the integer bin.
+* R19 b_max is the top level's width (the paper's b_n = b_max) and may be 4,
+      6 or 8 (Sec. 3.3 evaluates all three): RTN divides by 2^(b_max-1) - 1,
+      codes are offset by 2^(b_max-1), phi is 0 at b = b_max, and a stored
+      row holds b_max/u planes (tile_n * b_max / 8 bytes).
 """
 from __future__ import annotations
 
 import numpy as np
 
-B_MAX = 8
-OFFSET = 128          # z = -OFFSET * s  (R3)
+B_MAX = 8            # the default b_max; 4 and 6 are also stored (Sec. 3.3; R19)
+OFFSET = 128          # z = -OFFSET * s at b_max = 8; 2^(b_max-1) in general (R3)
 
 
 # ---------------------------------------------------------------------------
 # 1. RTN quantisation (Sec. 3.3 / Sec. 4; readings R3, R4, R5)
 # ---------------------------------------------------------------------------
-def rtn_quantize(W16: np.ndarray, group: int = 128):
-    """Quantise fp16 weights W[N, K] to 8-bit offset-binary codes.
+def rtn_quantize(W16: np.ndarray, group: int = 128, b_max: int = B_MAX):
+    """Quantise fp16 weights W[N, K] to b_max-bit offset-binary codes (R4):
+    s = fp16(fp32(max|w|) / (2^(b_max-1) - 1)), q = clamp(rint(w / s),
+    -2^(b_max-1), 2^(b_max-1) - 1) + 2^(b_max-1).
 
     Returns (codes uint8 [N, K], scales fp16 [K // group, N]).
     """
     W16 = np.asarray(W16, dtype=np.float16)
     N, K = W16.shape
     assert K % group == 0
+    half = 2 ** (b_max - 1)
     G = K // group
     w32 = W16.astype(np.float32).reshape(N, G, group)
     amax = np.max(np.abs(w32), axis=2)                                   # fp32 [N, G]
-    s16 = (amax / np.float32(127.0)).astype(np.float32).astype(np.float16)
+    s16 = (amax / np.float32(half - 1)).astype(np.float32).astype(np.float16)
     s32 = s16.astype(np.float32)
     zero = (s32 == 0.0)[:, :, None]
     with np.errstate(divide="ignore", invalid="ignore"):
         r = np.rint(w32 / s32[:, :, None])                 # fp32 IEEE divide, half-even
-    r = np.clip(np.where(zero, 0.0, r), -128.0, 127.0)     # a zero-scale group -> code 128
-    codes = (r.astype(np.int32) + OFFSET).astype(np.uint8)
+    r = np.clip(np.where(zero, 0.0, r), -half, half - 1)   # a zero-scale group -> code 2^(b_max-1)
+    codes = (r.astype(np.int32) + half).astype(np.uint8)
     return codes.reshape(N, K), np.ascontiguousarray(s16.T)
 
 
 # ---------------------------------------------------------------------------
 # 2./3. Nesting and reconstruction (Sec. 3.3; readings R1, R2, R10)
 # ---------------------------------------------------------------------------
-def nested_code(q: np.ndarray, b: int) -> np.ndarray:
-    """q_b: the integer formed by the b most significant bits of q."""
+def nested_code(q: np.ndarray, b: int, b_max: int = B_MAX) -> np.ndarray:
+    """q_b: the integer formed by the b most significant bits of the b_max-bit q."""
     q = np.asarray(q, dtype=np.int64)
-    return q >> (B_MAX - b)
+    return q >> (b_max - b)
 
 
-def midpoint_bias(b: int) -> float:
+def midpoint_bias(b: int, b_max: int = B_MAX) -> float:
     """phi for a b-bit read: 2^(b_max - b - 1), and 0 at full depth (R1)."""
-    if b >= B_MAX:
+    if b >= b_max:
         return 0.0
-    return float(2 ** (B_MAX - b - 1))
+    return float(2 ** (b_max - b - 1))
 
 
-def reconstruct(q: np.ndarray, s: np.ndarray, b: int) -> np.ndarray:
-    """w_hat = s * (q_b * 2^(b_max - b) + phi) + z with z = -128 s (float64).
+def reconstruct(q: np.ndarray, s: np.ndarray, b: int, b_max: int = B_MAX) -> np.ndarray:
+    """w_hat = s * (q_b * 2^(b_max - b) + phi) + z with z = -2^(b_max-1) s (float64).
 
     b = 0 is a skipped channel and reconstructs to exactly 0 (R2).
     """
     s = np.asarray(s, dtype=np.float64)
     if b == 0:
         return np.zeros(np.broadcast(np.asarray(q), s).shape, dtype=np.float64)
-    qb = nested_code(q, b).astype(np.float64)
-    z = -float(OFFSET) * s
-    return s * (qb * float(2 ** (B_MAX - b)) + midpoint_bias(b)) + z
+    qb = nested_code(q, b, b_max).astype(np.float64)
+    z = -float(2 ** (b_max - 1)) * s
+    return s * (qb * float(2 ** (b_max - b)) + midpoint_bias(b, b_max)) + z
 
 
 # ---------------------------------------------------------------------------
@@ -171,7 +178,9 @@ def assign_topk(x16: np.ndarray, counts) -> np.ndarray:
 # ---------------------------------------------------------------------------
 def dequantize(codes: np.ndarray, scales: np.ndarray, levels: np.ndarray,
                level_bits, group: int = 128) -> np.ndarray:
-    """W_hat[n, k] for one token's level map (float64 [N, K])."""
+    """W_hat[n, k] for one token's level map (float64 [N, K]).  The top
+    level's width is b_max (the paper's b_n = b_max, Sec. 3.1)."""
+    b_max = int(level_bits[-1])
     codes = np.asarray(codes)
     N, K = codes.shape
     s_full = np.repeat(np.asarray(scales, dtype=np.float16).astype(np.float64).T,
@@ -182,7 +191,7 @@ def dequantize(codes: np.ndarray, scales: np.ndarray, levels: np.ndarray,
         cols = np.nonzero(levels == lvl)[0]
         if cols.size == 0 or b == 0:
             continue
-        W[:, cols] = reconstruct(codes[:, cols], s_full[:, cols], int(b))
+        W[:, cols] = reconstruct(codes[:, cols], s_full[:, cols], int(b), b_max)
     return W
 
 
@@ -201,17 +210,17 @@ def vmm_batch(codes, scales, x16, levels, level_bits, group: int = 128) -> np.nd
                      for t in range(x16.shape[0])])
 
 
-def prefill(codes, scales, x16, group: int = 128) -> np.ndarray:
+def prefill(codes, scales, x16, group: int = 128, b_max: int = B_MAX) -> np.ndarray:
     """Stage-decoupled prefill (Sec. 3: the prompt is processed with the
     weights at the fixed top precision b_max; Sec. 4 "Prefill vs. Decoding
     Evaluation": unpack at b_max, dense matrix-matrix product).  Every channel
-    of every token is read at 8 bits, so W_hat = s (q - 128) (R1, R3) and
-    Y = X W_hat^T for the M tokens in x16 [M, K] (float64 [M, N])."""
+    of every token is read at b_max bits, so W_hat = s (q - 2^(b_max-1))
+    (R1, R3) and Y = X W_hat^T for the M tokens in x16 [M, K] (float64 [M, N])."""
     codes = np.asarray(codes)
     N, K = codes.shape
     s_full = np.repeat(np.asarray(scales, dtype=np.float16).astype(np.float64).T,
                        group, axis=1)                          # [N, K]
-    W = reconstruct(codes, s_full, B_MAX)
+    W = reconstruct(codes, s_full, b_max, b_max)
     X = np.atleast_2d(np.asarray(x16, dtype=np.float16)).astype(np.float64)
     return X @ W.T
 
@@ -224,41 +233,42 @@ def plane_bits_for(level_bits) -> int:
     return 2 if all(int(b) % 2 == 0 for b in level_bits) else 1
 
 
-def pack_codes(codes: np.ndarray, plane_bits: int, tile_n: int) -> np.ndarray:
-    """Pack codes[N, K] into the tile-major, row-prefix, bit-plane layout.
+def pack_codes(codes: np.ndarray, plane_bits: int, tile_n: int, b_max: int = B_MAX) -> np.ndarray:
+    """Pack b_max-bit codes[N, K] into the tile-major, row-prefix, bit-plane layout.
 
     Definition (written out bit by bit on purpose):
       * N is cut into tiles of ``tile_n`` outputs; tile t covers outputs
         t*tile_n .. t*tile_n + tile_n - 1;
-      * the row of (tile t, channel k) is ``tile_n`` bytes starting at byte
-        (t*K + k) * tile_n;
-      * it holds P = 8/u planes, most significant first; plane j (1-based)
+      * the row of (tile t, channel k) is R = tile_n*b_max/8 bytes starting at
+        byte (t*K + k) * R;
+      * it holds P = b_max/u planes, most significant first; plane j (1-based)
         starts at byte (j-1) * tile_n*u/8 of the row and holds, for local
-        output o, the u-bit field (q >> (8 - j*u)) & (2^u - 1) at bit o*u of
-        the plane (byte floor(o*u/8), bit (o*u) mod 8, little-endian bits).
+        output o, the u-bit field (q >> (b_max - j*u)) & (2^u - 1) at bit o*u
+        of the plane (byte floor(o*u/8), bit (o*u) mod 8, little-endian bits).
     """
     u = int(plane_bits)
     codes = np.asarray(codes, dtype=np.uint8)
     N, K = codes.shape
-    assert N % tile_n == 0 and 8 % u == 0
-    P = 8 // u
+    assert N % tile_n == 0 and 8 % u == 0 and b_max % u == 0
+    P = b_max // u
+    R = tile_n * b_max // 8
     plane_bytes = tile_n * u // 8
-    out = np.zeros(N * K, dtype=np.uint8)
+    out = np.zeros(N * K * b_max // 8, dtype=np.uint8)
     mask = (1 << u) - 1
     for t in range(N // tile_n):
         for k in range(K):
-            row = (t * K + k) * tile_n
+            row = (t * K + k) * R
             for o in range(tile_n):
                 q = int(codes[t * tile_n + o, k])
                 for j in range(1, P + 1):
-                    field = (q >> (8 - j * u)) & mask
+                    field = (q >> (b_max - j * u)) & mask
                     bit = o * u
                     byte = row + (j - 1) * plane_bytes + bit // 8
                     out[byte] |= field << (bit % 8)
     return out
 
 
-def pack_codes_fast(codes: np.ndarray, plane_bits: int, tile_n: int) -> np.ndarray:
+def pack_codes_fast(codes: np.ndarray, plane_bits: int, tile_n: int, b_max: int = B_MAX) -> np.ndarray:
     """Same bytes as ``pack_codes``, vectorised over outputs (for large tests).
 
     Equality with ``pack_codes`` is itself tested on small inputs.
@@ -266,14 +276,14 @@ def pack_codes_fast(codes: np.ndarray, plane_bits: int, tile_n: int) -> np.ndarr
     u = int(plane_bits)
     codes = np.asarray(codes, dtype=np.uint8)
     N, K = codes.shape
-    P = 8 // u
+    P = b_max // u
     per_byte = 8 // u
     T = N // tile_n
     c = codes.reshape(T, tile_n, K).transpose(0, 2, 1)            # [T, K, tile_n]
     mask = (1 << u) - 1
     planes = []
     for j in range(1, P + 1):
-        f = ((c >> (8 - j * u)) & mask).astype(np.uint16)          # [T, K, tile_n]
+        f = ((c >> (b_max - j * u)) & mask).astype(np.uint16)      # [T, K, tile_n]
         f = f.reshape(T, K, tile_n // per_byte, per_byte)
         byte = np.zeros(f.shape[:3], dtype=np.uint16)
         for e in range(per_byte):
@@ -283,7 +293,7 @@ def pack_codes_fast(codes: np.ndarray, plane_bits: int, tile_n: int) -> np.ndarr
 
 
 def unpack_prefix(packed: np.ndarray, N: int, K: int, plane_bits: int, tile_n: int,
-                  depth_bits: int) -> np.ndarray:
+                  depth_bits: int, b_max: int = B_MAX) -> np.ndarray:
     """Read the first depth_bits/u planes of every row and rebuild q_b [N, K]."""
     u = int(plane_bits)
     assert depth_bits % u == 0
@@ -291,7 +301,7 @@ def unpack_prefix(packed: np.ndarray, N: int, K: int, plane_bits: int, tile_n: i
     per_byte = 8 // u
     plane_bytes = tile_n * u // 8
     T = N // tile_n
-    rows = np.asarray(packed, dtype=np.uint8).reshape(T, K, tile_n)
+    rows = np.asarray(packed, dtype=np.uint8).reshape(T, K, tile_n * b_max // 8)
     q = np.zeros((T, K, tile_n), dtype=np.int64)
     mask = (1 << u) - 1
     for j in range(1, planes + 1):
