@@ -130,6 +130,23 @@ def copy_calibration(mib: int, reps: int):
     print(json.dumps({"copy_bytes_read": n, "copy_bytes_written": n, "reps": reps}), flush=True)
 
 
+BMAX_LEVELS = {6: inputs.LEVELS_D, 4: inputs.LEVELS_E}
+
+
+def workload(name: str, bmax: int):
+    """The named workload, with the level set of the stored width b_max
+    (codes quantised at b_max bits; the budget falls back to 3 bits when the
+    level set has no row for the workload's own budget)."""
+    wl = WORKLOADS[name]
+    if bmax == 8:
+        return name, wl
+    levels = BMAX_LEVELS[bmax]
+    budget = wl["budget"] if wl["budget"] in inputs.BUDGETS[levels] else 3
+    if name == "llama3-8b-prefill":
+        budget = bmax
+    return f"{name}-bmax{bmax}", dict(wl, levels=levels, budget=budget)
+
+
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -143,6 +160,8 @@ def parse():
     ap.add_argument("--n-layers", type=int, default=0, help="decoder layers (decode workload)")
     ap.add_argument("--prefill-tokens", type=int, default=0, help="prompt tokens M (prefill workload)")
     ap.add_argument("--layer", default=None, help="prefill workload: run only this projection")
+    ap.add_argument("--bmax", type=int, default=8, choices=(4, 6, 8),
+                    help="stored code width: 8 (levels {0,2,4,6,8}), 6 ({0,2,4,6}) or 4 ({0,2,4})")
     ap.add_argument("--tile-n", type=int, default=0)
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
     ap.add_argument("--vmm-only-reps", type=int, default=5)
@@ -191,7 +210,7 @@ def cpu_baseline(wl, p_bp, assign: str, tokens_sample: int):
 
     levels = wl["levels"]
     xs = make_inputs(wl, tokens_sample, 100)
-    codes = {name: orc.rtn_quantize(inputs.weights(N, K, wl["cfg"], li))
+    codes = {name: orc.rtn_quantize(inputs.weights(N, K, wl["cfg"], li), b_max=int(levels[-1]))
              for li, (name, K, N, _, _) in enumerate(wl["layers"])}
     ths = {}
     if assign == "threshold":
@@ -225,8 +244,9 @@ def run_decode(args, torch, g):
     has its own weights; the activations of each projection kind are shared
     by the layers (they only decide which bytes are read)."""
     dev = torch.device("cuda:0")
-    wl = WORKLOADS["llama3-8b-decode"]
+    wl_name, wl = workload("llama3-8b-decode", args.bmax)
     levels, layers = wl["levels"], wl["layers"]
+    bmax = int(levels[-1])
     L = args.n_layers or wl["n_layers"]
     B = args.batch
     if not 1 <= B <= 4:
@@ -242,7 +262,7 @@ def run_decode(args, torch, g):
     for li in range(L):
         per = {}
         for name, K, N, _, _ in layers:
-            codes = torch.randint(0, 256, (N, K), dtype=torch.uint8, device=dev, generator=gen)
+            codes = torch.randint(0, 1 << bmax, (N, K), dtype=torch.uint8, device=dev, generator=gen)
             sc = (torch.rand((N, K // 128), device=dev, generator=gen) * 4e-4 + 1e-4).half()
             per[name] = g.grinqh_pack(descs[name], codes=codes, scales=sc)
             del codes, sc
@@ -318,7 +338,7 @@ def run_decode(args, torch, g):
         "vs_baseline": None, "dtype": "u8 codes, fp16 x, f32 accumulate",
         "data": "synthetic (uniform random 8-bit codes and fp16 scales; Student-t(3) activations "
                 "with 1% x20 outlier channels; SiLU(g)*u for down projections)",
-        "config": {"workload": "llama3-8b-decode", "decoder_layers": L, "batch": B,
+        "config": {"workload": wl_name, "decoder_layers": L, "batch": B, "b_max": bmax,
                    "layers": {n: [K, N] for n, K, N, _, _ in layers}, "levels": list(levels),
                    "budget_bits": budget, "assignment": args.assign, "P_bp": list(p_bp),
                    "packed_weights_GB": round(packed_gb, 3), "achieved_avg_bits": main["achieved_avg_bits"]},
@@ -342,12 +362,15 @@ def cpu_baseline_prefill(wl, tokens_sample: int):
     with threadpool_limits(limits=1):
         dt = 0.0
         for li, (name, K, N, xin, kind) in enumerate(wl["layers"]):
+            bmax = int(wl["levels"][-1])
             codes = inputs.random_codes(N, K, wl["cfg"], li)
+            if bmax < 8:
+                codes = (codes & ((1 << bmax) - 1)).astype(np.uint8)
             sc = inputs.random_scales(N, K, 128, wl["cfg"], li).T.copy()
             gen = inputs.activations_swiglu if kind == "swiglu" else inputs.activations_t3
             x = gen(K, tokens_sample, wl["cfg"], 100 + xin)
             t0 = time.perf_counter()
-            orc.prefill(codes, sc, x)
+            orc.prefill(codes, sc, x, b_max=bmax)
             dt += time.perf_counter() - t0
             flops += 2 * tokens_sample * K * N
     return {"value": round(flops / dt / 1e12, 5), "unit": "TFLOP/s", "cores": 1, "kind": "oracle",
@@ -363,8 +386,9 @@ def run_prefill(args, torch, g):
     packed from codes; a plain fp16 GEMM (torch.mm on the unpacked weights,
     i.e. hipBLASLt) is timed on the same shapes as context."""
     dev = torch.device("cuda:0")
-    wl = WORKLOADS["llama3-8b-prefill"]
+    wl_name, wl = workload("llama3-8b-prefill", args.bmax)
     levels, layers = wl["levels"], wl["layers"]
+    bmax = int(levels[-1])
     if args.layer:
         layers = [l for l in layers if l[0] == args.layer]
         if not layers:
@@ -376,10 +400,10 @@ def run_prefill(args, torch, g):
     descs, packed, dense = {}, {}, {}
     for name, K, N, _, _ in layers:
         d = g.grinqh_resolve_desc(g.make_desc(K, N, levels, tile_n=args.tile_n))
-        codes = torch.randint(0, 256, (N, K), dtype=torch.uint8, device=dev, generator=gen)
+        codes = torch.randint(0, 1 << bmax, (N, K), dtype=torch.uint8, device=dev, generator=gen)
         sc = (torch.rand((N, K // 128), device=dev, generator=gen) * 4e-4 + 1e-4).half()
         descs[name], packed[name] = d, g.grinqh_pack(d, codes=codes, scales=sc)
-        w = (codes.float() - 128.0) * sc.float().repeat_interleave(128, dim=1)
+        w = (codes.float() - float(1 << (bmax - 1))) * sc.float().repeat_interleave(128, dim=1)
         dense[name] = w.t().contiguous().half()        # [K, N], for torch.mm(x, w)
         del codes, sc, w
     xs = {}
@@ -446,18 +470,18 @@ def run_prefill(args, torch, g):
     dom = max(layers, key=lambda l: layer_flops[l[0]])[0]
     value = step_flops / (ms_step * 1e-3) / 1e12
     out = {
-        "metric": "prefill TFLOP/s of one decoder layer at full 8-bit precision",
+        "metric": "prefill TFLOP/s of one decoder layer at full b_max precision",
         "value": round(value, 1), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(ms_step, 4), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "f16 x, f16 dequantised weights, f32 accumulate",
         "data": "synthetic (uniform random 8-bit codes and fp16 scales; N(0,1) and SiLU(g)*u activations)",
-        "config": {"workload": "llama3-8b-prefill", "tokens": M,
+        "config": {"workload": wl_name, "tokens": M, "b_max": bmax,
                    "layers": {n: [K, N] for n, K, N, _, _ in layers}, "levels": list(levels)},
         "per_layer": per_layer,
         "roofline": {"bound": "mfma", "achieved": per_layer[dom]["TFLOPs"], "peak": MFMA_F16_PEAK_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(per_layer[dom]["TFLOPs"] / MFMA_F16_PEAK_TFLOPS, 4),
                      "traffic": stored_traffic(None, None, None, sources=PREFILL_SOURCES,
-                                               path=os.path.join(PROFILES, f"k_prefill_traffic_llama3-8b-prefill_{dom}.md"))
+                                               path=os.path.join(PROFILES, f"k_prefill_traffic_{wl_name}_{dom}.md"))
                      if M == wl["tokens"] else None,
                      "kernel": f"k_prefill ({dom})"},
         "torch_fp16_dense": {"ms_per_step": round(ms_dense, 4),
@@ -490,7 +514,7 @@ def main():
         return run_prefill(args, torch, g)
 
     dev = torch.device("cuda:0")
-    wl = WORKLOADS[args.workload]
+    wl_name, wl = workload(args.workload, args.bmax)
     cfg, levels, layers = wl["cfg"], wl["levels"], wl["layers"]
     budget = args.budget if args.budget is not None else wl["budget"]
     p_bp = inputs.BUDGETS[levels][budget]
@@ -672,7 +696,7 @@ def main():
         "dtype": "u8 codes, fp16 x, f32 accumulate",
         "data": "synthetic (seeded N(0,0.02) weights RTN-quantised; Student-t(3) activations "
                 "with 1% x20 outlier channels; SiLU(g)*u for down projections)",
-        "config": {"workload": args.workload,
+        "config": {"workload": wl_name, "b_max": int(wl["levels"][-1]),
                    "layers": {n: [K, N] for n, K, N, _, _ in layers},
                    "tokens": T, "batch": 1, "levels": list(levels), "budget_bits": budget,
                    "assignment": main_mode, "P_bp": list(p_bp), "weight_copies": R,
@@ -682,7 +706,7 @@ def main():
         "per_layer": per_layer,
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                     "traffic": stored_traffic(args.workload, budget, main_mode)},
+                     "traffic": stored_traffic(wl_name, budget, main_mode)},
         "algorithmic_bytes_per_vmm": round(bytes_per_vmm, 1),
         "other_assignment": {
             "assignment": other, "ms_per_step": round(results[other]["ms_step"], 4),

@@ -24,16 +24,19 @@
  *   - Calls are thread-safe; the error message is per thread.
  *
  * Packed layout (the contract between grinqh_pack and grinqh_vmm)
- *   u (plane_bits) in {1, 2}; P = 8/u planes; T (tile_n) outputs per tile.
- *   codes buffer: (N/T) tiles x K rows x T bytes = K*N bytes.
- *   Row (tile t, channel k) starts at byte (t*K + k)*T.  Plane j (1-based,
+ *   b_max (the top level's bits) in {4, 6, 8}: codes q are b_max-bit offset
+ *   binary, w_hat = s*(q - 2^(b_max-1)) at full depth (Sec. 3.3 stores b_max
+ *   = 4, 6 or 8).  u (plane_bits) in {1, 2}; P = b_max/u planes; T (tile_n)
+ *   outputs per tile; R = T*b_max/8 bytes per stored row.
+ *   codes buffer: (N/T) tiles x K rows x R bytes = K*N*b_max/8 bytes.
+ *   Row (tile t, channel k) starts at byte (t*K + k)*R.  Plane j (1-based,
  *   j = 1 most significant) starts at byte (j-1)*T*u/8 of the row and holds,
- *   for local output o = n - t*T, the field (q >> (8 - j*u)) & (2^u - 1) at
- *   bit o*u of the plane (byte floor(o*u/8), bit (o*u) % 8, little-endian).
+ *   for local output o = n - t*T, the field (q >> (b_max - j*u)) & (2^u - 1)
+ *   at bit o*u of the plane (byte floor(o*u/8), bit (o*u) % 8, little-endian).
  *   Reading b bits of a channel therefore reads the first b*T/8 bytes of its
  *   row in every tile: a contiguous prefix, a multiple of 64 bytes.
  *   scales buffer: fp16 [K/128][N], the scale of group g for output n at
- *   index g*N + n.  Codes are offset binary: w_hat = s*(q - 128) at 8 bits.
+ *   index g*N + n.
  */
 #ifndef GRINQH_H
 #define GRINQH_H
@@ -68,7 +71,8 @@ typedef struct {
   int32_t group;      /* quantisation group along K; must be 128 */
   int32_t n_levels;   /* number of levels n+1 including level 0; 2..9 */
   uint8_t level_bits[GRINQH_MAX_LEVELS];
-                      /* b_0 = 0 < b_1 < ... < b_n = 8 (Sec. 3.1: the set B);
+                      /* b_0 = 0 < b_1 < ... < b_n = b_max (Sec. 3.1: the set
+                         B); b_max in {4, 6, 8} is the stored code width;
                          every b_i a multiple of plane_bits */
   uint8_t reserved_[3];
   int32_t plane_bits; /* u: 0 = auto (2 if every b_i is even, else 1); or 1, 2 */
@@ -83,20 +87,22 @@ enum { GRINQH_VMM_ACCUMULATE = 1 };
  * validating it.  Host only.  Every other entry point resolves the same way. */
 GRINQH_API int grinqh_resolve_desc(const grinqh_layer_desc* in, grinqh_layer_desc* out);
 
-/* Sizes of the packed buffers of a layer (host only): codes K*N bytes,
- * scales 2*(K/128)*N bytes. */
+/* Sizes of the packed buffers of a layer (host only): codes K*N*b_max/8
+ * bytes, scales 2*(K/128)*N bytes. */
 GRINQH_API int grinqh_packed_bytes(const grinqh_layer_desc* desc, size_t* codes_bytes,
                         size_t* scales_bytes);
 
 /* Offline quantise + nest + pack (Sec. 3.3, App. C.1).
  *   src_kind GRINQH_SRC_FP16_RTN: src = fp16 W[N][K] (torch Linear.weight
- *     layout), src_scales = NULL.  Symmetric RTN per (output, group of 128
- *     channels): s = fp16_rne(fp32(max|w|)/127), q = clamp(rne(w/s), -128, 127)
- *     + 128; a group with s == 0 gets q = 128.  W must be finite.
- *   src_kind GRINQH_SRC_CODES_U8: src = uint8 codes q[N][K] from any base
- *     quantiser with the same offset-binary convention, src_scales = fp16
- *     s[N][K/128] (the method is quantisation-agnostic, Sec. 3.3).
- *   Outputs: packed_codes (K*N bytes, layout above), packed_scales
+ *     layout), src_scales = NULL.  Symmetric RTN at b_max bits per (output,
+ *     group of 128 channels), with h = 2^(b_max-1): s = fp16_rne(fp32(max|w|)
+ *     / (h - 1)), q = clamp(rne(w/s), -h, h - 1) + h; a group with s == 0
+ *     gets q = h.  W must be finite.
+ *   src_kind GRINQH_SRC_CODES_U8: src = uint8 codes q[N][K] (q < 2^b_max;
+ *     higher bits are ignored) from any base quantiser with the same
+ *     offset-binary convention, src_scales = fp16 s[N][K/128] (the method is
+ *     quantisation-agnostic, Sec. 3.3).
+ *   Outputs: packed_codes (K*N*b_max/8 bytes, layout above), packed_scales
  *   (fp16 [K/128][N]).  Inputs and outputs must not overlap. */
 GRINQH_API int grinqh_pack(const grinqh_layer_desc* desc, int src_kind, const void* src,
                 const void* src_scales, void* packed_codes, void* packed_scales,
@@ -146,10 +152,10 @@ GRINQH_API int grinqh_assign(const grinqh_layer_desc* desc, int mode, const void
                   void* workspace, size_t ws_bytes, void* stream);
 
 /* Nested-precision decode VMM (Sec. 3.3 reconstruction; App. C.1).
- *   y[t][n] = sum_k x[t][k] * w_hat(k, n), with w_hat = s*(q_b*2^(8-b) + phi
- *   - 128) for the b = level_bits[level_map[t][k]] most significant bits q_b
- *   of the code, phi = 2^(7-b) for 0 < b < 8, phi = 0 at b = 8, and channels
- *   at level 0 skipped.  Only the first b*T/8 bytes of each of a channel's
+ *   y[t][n] = sum_k x[t][k] * w_hat(k, n), with w_hat = s*(q_b*2^(b_max-b)
+ *   + phi - 2^(b_max-1)) for the b = level_bits[level_map[t][k]] most
+ *   significant bits q_b of the code, phi = 2^(b_max-b-1) for 0 < b < b_max,
+ *   phi = 0 at b = b_max, and channels at level 0 skipped.  Only the first b*T/8 bytes of each of a channel's
  *   rows are read; for B > 1 the deepest level over the B tokens is read once
  *   and each token uses its own prefix of it.
  *   x: fp16 [B][K]; level_map: uint8 [B][K], values < n_levels (a larger
@@ -174,8 +180,8 @@ GRINQH_API int grinqh_vmm_threshold(const grinqh_layer_desc* desc, const void* p
 
 /* Prefill, the stage-decoupled dense path (Sec. 3: prefill reads the weights
  * at the fixed top precision; Sec. 4 "Prefill vs. Decoding Evaluation"): for
- * M tokens at once, every channel at all 8 bits,
- *   Y[m][n] = sum_k X[m][k] * w_hat[n][k],  w_hat = s[k/128][n] * (q[n][k] - 128),
+ * M tokens at once, every channel at all b_max bits,
+ *   Y[m][n] = sum_k X[m][k] * w_hat[n][k],  w_hat = s[k/128][n] * (q[n][k] - 2^(b_max-1)),
  * with each w_hat rounded once to fp16 (the dequantised weight of a dense
  * fp16 GEMM), fp16 x fp16 products and fp32 accumulation: per element
  * |Y - exact| <= (2^-11 + K 2^-24) sum_k |X[m][k]| |w_hat[n][k]|.  Reads the

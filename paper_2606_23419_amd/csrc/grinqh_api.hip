@@ -39,7 +39,9 @@ static int resolve(const grinqh_layer_desc* d, Layer* L, grinqh_layer_desc* out)
   const int nl = d->n_levels;
   if (nl < 2 || nl > kMaxLevels) return fail(GRINQH_EINVAL, "n_levels=%d outside 2..%d", nl, kMaxLevels);
   if (d->level_bits[0] != 0) return fail(GRINQH_EINVAL, "level_bits[0] must be 0 (the skip level)");
-  if (d->level_bits[nl - 1] != 8) return fail(GRINQH_EINVAL, "the top level must read all 8 bits");
+  const int bmax = d->level_bits[nl - 1];
+  if (bmax != 4 && bmax != 6 && bmax != 8)
+    return fail(GRINQH_EUNSUPPORTED, "the top level is the stored width b_max and must be 4, 6 or 8 (got %d)", bmax);
   bool all_even = true;
   for (int i = 1; i < nl; ++i) {
     if (d->level_bits[i] <= d->level_bits[i - 1])
@@ -75,7 +77,9 @@ static int resolve(const grinqh_layer_desc* d, Layer* L, grinqh_layer_desc* out)
     if (d->N % T) return fail(GRINQH_EINVAL, "N=%d is not a multiple of tile_n=%d", d->N, T);
   }
   if (L) {
-    L->K = d->K; L->N = d->N; L->n_levels = nl; L->u = u; L->P = 8 / u; L->T = T;
+    L->K = d->K; L->N = d->N; L->n_levels = nl; L->u = u; L->bmax = bmax; L->P = bmax / u; L->T = T;
+    L->RB = T * bmax / 8;
+    L->sfac = ldexpf(1.0f, bmax - 8);
     L->tiles = d->N / T; L->groups = d->K / kGroup;
     L->planes_packed = 0;
     for (int i = 0; i < kMaxLevels; ++i) {
@@ -122,7 +126,7 @@ int grinqh_packed_bytes(const grinqh_layer_desc* desc, size_t* codes_bytes, size
   int st = resolve(desc, &L, nullptr);
   if (st) return st;
   if (!codes_bytes || !scales_bytes) return fail(GRINQH_EINVAL, "output pointers are NULL");
-  *codes_bytes = (size_t)L.K * (size_t)L.N;
+  *codes_bytes = (size_t)L.K * (size_t)L.N * (size_t)L.bmax / 8;
   *scales_bytes = (size_t)L.groups * (size_t)L.N * 2;
   return GRINQH_OK;
 }

@@ -17,8 +17,11 @@ constexpr int kMaxB = 4;          // tokens per VMM call
 struct Layer {
   int K, N, n_levels;
   int u;            // plane width in bits (1 or 2)
-  int P;            // number of planes, 8/u
+  int bmax;         // stored code width b_max (the top level's bits): 4, 6 or 8
+  int P;            // number of stored planes, bmax/u
   int T;            // outputs per tile
+  int RB;           // bytes of one stored row, T * bmax / 8
+  float sfac;       // 2^(bmax - 8): kernels work in 8-bit code units
   int tiles;        // N / T
   int groups;       // K / 128
   int bits[kMaxLevels];    // b_l

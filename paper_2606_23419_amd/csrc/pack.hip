@@ -8,9 +8,11 @@
 
 namespace grinqh {
 
-// s = fp16_rne(fp32(max|w|) / 127) per (output n, group g), written [g][n].
+// s = fp16_rne(fp32(max|w|) / qmax) per (output n, group g), written [g][n];
+// qmax = 2^(b_max-1) - 1 (127 at 8 bits).
 __global__ __launch_bounds__(256) void k_rtn_scales(const uint16_t* __restrict__ W,
-                                                    uint16_t* __restrict__ scales, int N, int K) {
+                                                    uint16_t* __restrict__ scales, int N, int K,
+                                                    float qmax) {
   const int G = K / kGroup;
   const long wave = ((long)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
   const int lane = threadIdx.x & 63;
@@ -19,7 +21,7 @@ __global__ __launch_bounds__(256) void k_rtn_scales(const uint16_t* __restrict__
   const uint16_t* p = W + (size_t)n * K + (size_t)g * kGroup;
   float a = fmaxf(fabsf(h2f(p[lane])), fabsf(h2f(p[lane + 64])));
   for (int off = 32; off > 0; off >>= 1) a = fmaxf(a, __shfl_xor(a, off));
-  if (lane == 0) scales[(size_t)g * N + n] = f2h_rn(__fdiv_rn(a, 127.0f));
+  if (lane == 0) scales[(size_t)g * N + n] = f2h_rn(__fdiv_rn(a, qmax));
 }
 
 // Externally quantised codes: scales arrive [n][g] and are stored [g][n].
@@ -31,11 +33,12 @@ __global__ __launch_bounds__(256) void k_transpose_scales(const uint16_t* __rest
   dst[i] = src[(size_t)n * G + g];
 }
 
+// b_max-bit codes (b_max = L.bmax), L.P = b_max/U planes per row of L.RB bytes.
 template <int U>
 __global__ __launch_bounds__(256) void k_pack(const void* __restrict__ src, int from_fp16,
                                               const uint16_t* __restrict__ scales,
                                               uint8_t* __restrict__ out, Layer L) {
-  constexpr int P = 8 / U;
+  constexpr int P = 8 / U;              // planes of the widest (8-bit) code
   constexpr int WORDS = U;              // 32 outputs * U bits = U dwords per plane
   constexpr uint32_t MASK = (1u << U) - 1u;
   const int chunks = L.T / 32;
@@ -54,6 +57,8 @@ __global__ __launch_bounds__(256) void k_pack(const void* __restrict__ src, int 
 #pragma unroll
     for (int w = 0; w < WORDS; ++w) plane[j][w] = 0u;
 
+  const int half = 1 << (L.bmax - 1);
+  const float lo = (float)-half, hi = (float)(half - 1);
 #pragma unroll 4
   for (int e = 0; e < 32; ++e) {
     const int n = t * L.T + c * 32 + e;
@@ -62,15 +67,18 @@ __global__ __launch_bounds__(256) void k_pack(const void* __restrict__ src, int 
       const float s = h2f(scales[(size_t)g * L.N + n]);
       const float w = h2f(((const uint16_t*)src)[(size_t)n * L.K + k]);
       if (s == 0.0f) {
-        q = 128u;
+        q = (uint32_t)half;
       } else {
         float rq = rintf(__fdiv_rn(w, s));
-        rq = fminf(fmaxf(rq, -128.0f), 127.0f);
-        q = (uint32_t)((int)rq + 128);
+        rq = fminf(fmaxf(rq, lo), hi);
+        q = (uint32_t)((int)rq + half);
       }
     } else {
       q = ((const uint8_t*)src)[(size_t)n * L.K + k];
     }
+    // left-align the b_max-bit code in 8 bits: plane j's field is then the
+    // same bit slice for every b_max (bits above b_max of a given code drop out)
+    q = (q << (8 - L.bmax)) & 0xFFu;
     const int bit = e * U;
 #pragma unroll
     for (int j = 0; j < P; ++j) {
@@ -78,10 +86,11 @@ __global__ __launch_bounds__(256) void k_pack(const void* __restrict__ src, int 
       plane[j][bit >> 5] |= field << (bit & 31);
     }
   }
-  uint8_t* row = out + ((size_t)t * L.K + k) * L.T;
+  uint8_t* row = out + ((size_t)t * L.K + k) * L.RB;
   const int plane_bytes = L.T * U / 8;
 #pragma unroll
   for (int j = 0; j < P; ++j) {
+    if (j >= L.P) break;
     uint32_t* dst = (uint32_t*)(row + (size_t)j * plane_bytes + (size_t)c * 32 * U / 8);
 #pragma unroll
     for (int w = 0; w < WORDS; ++w) dst[w] = plane[j][w];
@@ -95,7 +104,8 @@ int launch_pack(const Layer& L, int src_kind, const void* src, const void* src_s
     const long waves = (long)L.N * L.groups;
     const long blocks = (waves * 64 + 255) / 256;
     hipLaunchKernelGGL(k_rtn_scales, dim3((unsigned)blocks), dim3(256), 0, s,
-                       (const uint16_t*)src, (uint16_t*)packed_scales, L.N, L.K);
+                       (const uint16_t*)src, (uint16_t*)packed_scales, L.N, L.K,
+                       (float)((1 << (L.bmax - 1)) - 1));
   } else {
     const long n = (long)L.N * L.groups;
     hipLaunchKernelGGL(k_transpose_scales, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s,

@@ -147,20 +147,24 @@ __global__ __launch_bounds__(kThreadsPF) void k_prefill(const uint8_t* __restric
           (__attribute__((address_space(3))) void*)&sx[8 * kBK * (4 * i + wave)], 16, 0, 0);
   };
 
-  // Code staging: the tile's part of a channel row is BN bytes (every plane's
-  // BN u / 8 bytes).  Staged chunk slot v of row r (v = plane * PPP + piece)
-  // sits at position v ^ ((r / CPT) & 7) of the row, so the word reads below
-  // (8 channel groups x 8 output chunks per instruction) hit distinct banks.
-  const uint8_t* wtile = codes + (size_t)tile * K * T + o0 * U / 8;
+  // Code staging: the tile's part of a channel row is BN bytes at 8 bits
+  // (every plane's BN u / 8 bytes).  Staged chunk slot v of row r (v = plane *
+  // PPP + piece) sits at position v ^ ((r / CPT) & 7) of the row, so the word
+  // reads below (8 channel groups x 8 output chunks per instruction) hit
+  // distinct banks.  A code narrower than 8 bits (b_max = 4, 6) has only L.P
+  // planes in its stored row of L.RB bytes: the slots of the missing planes
+  // copy plane 1 again (in bounds) and are read as zero.
+  const uint8_t* wtile = codes + (size_t)tile * K * L.RB + o0 * U / 8;
   int wsrc[WI];
 #pragma unroll
   for (int i = 0; i < WI; ++i) {
     const int q = 64 * (4 * i + wave) + lane;
     const int r = q / RCH, v = (q % RCH) ^ ((r / CPT) & 7);
-    wsrc[i] = r * T + (v / PPP) * (T * U / 8) + 16 * (v % PPP);
+    const int pl = v / PPP;
+    wsrc[i] = r * L.RB + (pl < L.P ? pl : 0) * (T * U / 8) + 16 * (v % PPP);
   }
   auto copy_w = [&](int st, uint8_t* sp) __attribute__((always_inline)) {
-    const uint8_t* base = wtile + (size_t)st * kBK * T;
+    const uint8_t* base = wtile + (size_t)st * kBK * L.RB;
 #pragma unroll
     for (int i = 0; i < WI; ++i)
       __builtin_amdgcn_global_load_lds(
@@ -177,19 +181,22 @@ __global__ __launch_bounds__(kThreadsPF) void k_prefill(const uint8_t* __restric
     R.s[0] = sg[0];
     R.s[1] = sg[1];
   };
+  const int np = L.P;
   auto read_w = [&](const uint8_t* sp, WRegs<U, CPT>& R) __attribute__((always_inline)) {
 #pragma unroll
     for (int r = 0; r < CPT; ++r) {
       const int row = cg * CPT + r;
 #pragma unroll
       for (int p = 0; p < kWords; ++p) {
+        uint32_t wd;
         if constexpr (U == 2) {
           const int v = (p * PPP + (j >> 2)) ^ (cg & 7);
-          R.w[r][p] = *(const uint32_t*)&sp[16 * (row * RCH + v) + 4 * (j & 3)];
+          wd = *(const uint32_t*)&sp[16 * (row * RCH + v) + 4 * (j & 3)];
         } else {
           const int v = (p * PPP + (j >> 3)) ^ (cg & 7);
-          R.w[r][p] = *(const uint16_t*)&sp[16 * (row * RCH + v) + 2 * (j & 7)];
+          wd = *(const uint16_t*)&sp[16 * (row * RCH + v) + 2 * (j & 7)];
         }
+        R.w[r][p] = p < np ? wd : 0u;   // planes past b_max are zero
       }
     }
   };
@@ -313,7 +320,8 @@ __global__ __launch_bounds__(kThreadsPF) void k_prefill(const uint8_t* __restric
 #pragma unroll
       for (int b = 0; b < NB; ++b) {
         float* dst = y + (size_t)m * N + n0 + wn + 32 * b + (lane & 31);
-        *dst = accumulate ? *dst + acc[a][b][e] : acc[a][b][e];
+        const float v = acc[a][b][e] * L.sfac;   // 8-bit code units -> b_max units (exact)
+        *dst = accumulate ? *dst + v : v;
       }
     }
 }

@@ -19,9 +19,10 @@ namespace grinqh {
 
 constexpr int kVmmThreads = 256;
 
-__device__ __forceinline__ float midpoint_minus_offset(int b) {
-  // phi_b - 128 with phi_b = 2^(7-b) for 0 < b < 8 and phi_8 = 0
-  return (b < 8 ? (float)(1 << (7 - b)) : 0.0f) - 128.0f;
+__device__ __forceinline__ float midpoint_minus_offset(int b, int bmax) {
+  // phi_b - 128 in 8-bit code units: phi_b = 2^(7-b) for 0 < b < b_max and
+  // 0 at b = b_max (a b_max-bit code is the top b_max bits of an 8-bit one)
+  return (b < bmax ? (float)(1 << (7 - b)) : 0.0f) - 128.0f;
 }
 
 __global__ __launch_bounds__(256) void k_zero(float* __restrict__ y, long n) {
@@ -72,7 +73,7 @@ __global__ __launch_bounds__(kVmmThreads) void k_vmm_v0(
       if (lvl == 0) continue;
       const int d = level_planes(L.planes_packed, lvl);
       const int b = d * U;
-      const uint8_t* row = codes + ((size_t)t * L.K + k) * L.T;
+      const uint8_t* row = codes + ((size_t)t * L.K + k) * L.RB;
       uint32_t code[16];
 #pragma unroll
       for (int e = 0; e < 16; ++e) code[e] = 0u;
@@ -86,7 +87,7 @@ __global__ __launch_bounds__(kVmmThreads) void k_vmm_v0(
       const int sh = 8 - b;
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[e] = fmaf(xv, (float)(code[e] << sh), acc[e]);
-      beta = fmaf(xv, midpoint_minus_offset(b), beta);
+      beta = fmaf(xv, midpoint_minus_offset(b, L.bmax), beta);
     }
     const uint16_t* sg = scales + (size_t)g * L.N + (size_t)t * L.T + li * 16;
 #pragma unroll
@@ -100,7 +101,7 @@ __global__ __launch_bounds__(kVmmThreads) void k_vmm_v0(
   for (int o = threadIdx.x; o < L.T; o += kVmmThreads) {
     float s = 0.0f;
     for (int q = 0; q < nlg; ++q) s += red[q * L.T + o];
-    atomicAdd(&yt[o], s);
+    atomicAdd(&yt[o], s * L.sfac);   // 8-bit code units -> b_max units
   }
 }
 

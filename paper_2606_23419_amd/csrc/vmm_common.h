@@ -54,8 +54,11 @@ __device__ __forceinline__ float offset_factor(int e) {
   return (m == 4 || m == 7) ? 0.0625f : ((m == 1 || m == 3 || m == 6) ? 0.25f : 1.0f);
 }
 
-__device__ __forceinline__ float phi_minus_offset(int b) {
-  return (b < 8 ? (float)(1 << (7 - b)) : 0.0f) - 128.0f;
+// phi_b - 128 in 8-bit code units for a b-bit read of a b_max-bit code: a
+// b_max-bit code is the top b_max bits of an 8-bit one, its phi_b is
+// 2^(7-b) in those units, and 0 at b = b_max (nothing dropped).
+__device__ __forceinline__ float phi_minus_offset(int b, int bmax) {
+  return (b < bmax ? (float)(1 << (7 - b)) : 0.0f) - 128.0f;
 }
 
 template <int V>

@@ -132,8 +132,8 @@ __global__ __launch_bounds__(kThreads) void k_vmm_dot2(
       db[b] = level_planes(L.planes_packed, lb);
       D0 = max(D0, da[b]);
       D1 = max(D1, db[b]);
-      beta[b] = (la ? fa * phi_minus_offset(2 * da[b]) : 0.0f) +
-                (lb ? fb * phi_minus_offset(2 * db[b]) : 0.0f);
+      beta[b] = (la ? fa * phi_minus_offset(2 * da[b], L.bmax) : 0.0f) +
+                (lb ? fb * phi_minus_offset(2 * db[b], L.bmax) : 0.0f);
     }
     const int cnt = D0 + D1;
     const int np = (cnt + 1) >> 1;
@@ -154,8 +154,8 @@ __global__ __launch_bounds__(kThreads) void k_vmm_dot2(
       const int rb = ib < D0 ? 0 : 1, jb = has_b ? (ib < D0 ? ib + 1 : ib - D0 + 1) : ja;
       const int rbb = has_b ? rb : ra;
       uint32_t* d = s_pairs[gg][pos + q];
-      d[0] = (uint32_t)((k0 + ra) * T + (ja - 1) * (T / 4));
-      d[1] = (uint32_t)((k0 + rbb) * T + (jb - 1) * (T / 4));
+      d[0] = (uint32_t)((k0 + ra) * L.RB + (ja - 1) * (T / 4));
+      d[1] = (uint32_t)((k0 + rbb) * L.RB + (jb - 1) * (T / 4));
       d[2] = ((uint32_t)(29 - 2 * ja) << 10) | ((uint32_t)(29 - 2 * jb) << 26);
 #pragma unroll
       for (int b = 0; b < NB; ++b) {
@@ -202,7 +202,7 @@ __global__ __launch_bounds__(kThreads) void k_vmm_dot2(
   // of the next batch are in flight while the current one is consumed, across
   // group boundaries too.  A group with no pairs still gets one (empty) batch
   // so its epilogue runs and the scale prefetch advances.
-  const uint8_t* tile = codes + (size_t)t * L.K * T + li * 4 * V;
+  const uint8_t* tile = codes + (size_t)t * L.K * L.RB + li * 4 * V;
   float yp[NB][NACC], acc[NB][NACC], off[NB];
 #pragma unroll
   for (int b = 0; b < NB; ++b) {
@@ -348,7 +348,7 @@ __global__ __launch_bounds__(kThreads) void k_vmm_dot2(
     float v = 0.0f;
 #pragma unroll
     for (int w = 0; w < kWaves; ++w) v += s_red[b][w][o];
-    atomicAdd(&y[(size_t)b * L.N + (size_t)t * T + o], v);
+    atomicAdd(&y[(size_t)b * L.N + (size_t)t * T + o], v * L.sfac);   // 8-bit units -> b_max units
   }
 }
 

@@ -120,7 +120,7 @@ __global__ __launch_bounds__(kThreads) void k_vmm_pp(
     constexpr int kLines = kGroup * kLinesPerRow / kRowsPerLine;   // <= kThreads
     const int i = tid % kLines;   // threads past kLines repeat a line
     const int r = (i / kLinesPerRow) * kRowsPerLine, c = i % kLinesPerRow;
-    const uint8_t* a = codes + (size_t)t * L.K * T + (size_t)(g0 * kGroup + r) * T + c * 128;
+    const uint8_t* a = codes + (size_t)t * L.K * L.RB + (size_t)(g0 * kGroup + r) * L.RB + c * 128;
     asm volatile("global_load_dword %0, %1, off" : "=v"(pf) : "v"(a) : "memory");
   }
 
@@ -165,7 +165,8 @@ __global__ __launch_bounds__(kThreads) void k_vmm_pp(
       lb = min((int)(ll >> 8), n_top);
     }
     const int da = level_planes(L.planes_packed, la), db = level_planes(L.planes_packed, lb);
-    const float beta = (la ? fa * phi_minus_offset(2 * da) : 0.0f) + (lb ? fb * phi_minus_offset(2 * db) : 0.0f);
+    const float beta = (la ? fa * phi_minus_offset(2 * da, L.bmax) : 0.0f) +
+                       (lb ? fb * phi_minus_offset(2 * db, L.bmax) : 0.0f);
     const int nda = da >> 1, ndb = db >> 1;      // doubles of each row
     const int nsa = da & 1, nsb = db & 1;        // singles of each row
     const int nd = nda + ndb, ns = nsa + nsb;
@@ -191,7 +192,7 @@ __global__ __launch_bounds__(kThreads) void k_vmm_pp(
       if (q >= nd) break;
       const bool ra = q < nda;
       const int j = 2 * (ra ? q : q - nda) + 1;               // first plane of the pair
-      const uint32_t off = (uint32_t)((k0 + (ra ? 0 : 1)) * T + (j - 1) * PLANE);
+      const uint32_t off = (uint32_t)((k0 + (ra ? 0 : 1)) * L.RB + (j - 1) * PLANE);
       const int i = dpos + q, u = i >> 1, h = i & 1;
       U[u * 8 + h] = off;
       U[u * 8 + 4 + h] = off + PLANE;
@@ -203,7 +204,7 @@ __global__ __launch_bounds__(kThreads) void k_vmm_pp(
       if (q >= ns) break;
       const bool ra = (q == 0) && nsa;
       const int j = ra ? da : db;                             // the odd last plane
-      const uint32_t off = (uint32_t)((k0 + (ra ? 0 : 1)) * T + (j - 1) * PLANE);
+      const uint32_t off = (uint32_t)((k0 + (ra ? 0 : 1)) * L.RB + (j - 1) * PLANE);
       const int i = spos + q, u = pad_du + (i >> 2), sub = (i >> 1) & 1, h = i & 1;
       U[u * 8 + 4 * sub + h] = off;
       reinterpret_cast<uint16_t*>(&U[u * 8 + 4 * sub + 2])[h] = (uint16_t)((29 - 2 * j) << 10);
@@ -240,7 +241,7 @@ __global__ __launch_bounds__(kThreads) void k_vmm_pp(
   // ---- main loop: lane group lg takes units lg, lg + kLaneGroups, ... of
   // each batch; the (group, batch) sequence runs through four register sets,
   // three batches in flight while one is consumed.
-  const uint8_t* tile = codes + (size_t)t * L.K * T;
+  const uint8_t* tile = codes + (size_t)t * L.K * L.RB;
   const uint32_t li4 = (uint32_t)li * 4u;
   float yp[16], acc[16], off_d = 0.0f, off_s = 0.0f;
 #pragma unroll
@@ -367,7 +368,7 @@ loop_done:
     float v = 0.0f;
 #pragma unroll
     for (int w = 0; w < kWaves; ++w) v += s_red[w][o];
-    atomicAdd(&y[(size_t)t * T + o], v);
+    atomicAdd(&y[(size_t)t * T + o], v * L.sfac);   // 8-bit code units -> b_max units
   }
   if constexpr (PREFETCH) asm volatile("s_waitcnt vmcnt(0)" : "+v"(pf)::"memory");
 }
@@ -385,7 +386,7 @@ void launch_pp(dim3 grid, hipStream_t s, const void* codes, const void* scales, 
 bool vmm_pp_supported(const Layer& L, int B) {
   // byte offsets inside a tile are 32-bit
   return B == 1 && L.u == 2 && (L.T == 256 || L.T == 512 || L.T == 1024) &&
-         (long long)L.K * L.T < (1ll << 31);
+         (long long)L.K * L.RB < (1ll << 31);
 }
 
 int launch_vmm_pp(const Layer& L, const void* codes, const void* scales, const void* x,

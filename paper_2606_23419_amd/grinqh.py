@@ -249,7 +249,7 @@ def grinqh_vmm(desc: LayerDesc, packed_codes, packed_scales, x, level_map, y=Non
     if level_map.dim() == 1:
         level_map = level_map.view(1, -1)
     B = int(x.shape[0])
-    cp = _dev(packed_codes, torch.uint8, "packed_codes", (rd.K * rd.N,))
+    cp = _dev(packed_codes, torch.uint8, "packed_codes", (rd.K * rd.N * rd.level_bits[rd.n_levels - 1] // 8,))
     sp = _dev(packed_scales, torch.float16, "packed_scales", (rd.K // 128, rd.N))
     xp = _dev(x, torch.float16, "x", (B, rd.K))
     lp = _dev(level_map, torch.uint8, "level_map", (B, rd.K))
@@ -270,7 +270,7 @@ def grinqh_vmm_threshold(desc: LayerDesc, packed_codes, packed_scales, x, thresh
     if x.dim() == 1:
         x = x.view(1, -1)
     B = int(x.shape[0])
-    cp = _dev(packed_codes, torch.uint8, "packed_codes", (rd.K * rd.N,))
+    cp = _dev(packed_codes, torch.uint8, "packed_codes", (rd.K * rd.N * rd.level_bits[rd.n_levels - 1] // 8,))
     sp = _dev(packed_scales, torch.float16, "packed_scales", (rd.K // 128, rd.N))
     xp = _dev(x, torch.float16, "x", (B, rd.K))
     lo = _dev(level_map_out, torch.uint8, "level_map_out", (B, rd.K)) \
@@ -292,7 +292,7 @@ def grinqh_prefill(desc: LayerDesc, packed_codes, packed_scales, x, y=None,
     if x.dim() == 1:
         x = x.view(1, -1)
     M = int(x.shape[0])
-    cp = _dev(packed_codes, torch.uint8, "packed_codes", (rd.K * rd.N,))
+    cp = _dev(packed_codes, torch.uint8, "packed_codes", (rd.K * rd.N * rd.level_bits[rd.n_levels - 1] // 8,))
     sp = _dev(packed_scales, torch.float16, "packed_scales", (rd.K // 128, rd.N))
     xp = _dev(x, torch.float16, "x", (M, rd.K))
     if y is None:

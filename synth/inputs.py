@@ -92,6 +92,8 @@ def activations_swiglu(K: int, tokens: int, config: int = 1, layer: int = 0, see
 LEVELS_A = (0, 2, 4, 8)
 LEVELS_B = (0, 2, 4, 6, 8)
 LEVELS_C = (0, 2, 3, 4, 8)
+LEVELS_D = (0, 2, 4, 6)       # b_max = 6
+LEVELS_E = (0, 2, 4)          # b_max = 4
 
 BUDGETS = {
     LEVELS_A: {
@@ -111,6 +113,17 @@ BUDGETS = {
         2: (3000, 4000, 2000, 500, 500),
         3: (2000, 3000, 2000, 1500, 1500),
         4: (2000, 1000, 2000, 2000, 3000),
+    },
+    # rows of the same sweep table, b_max = 6 and b_max = 4 columns
+    LEVELS_D: {
+        3: (2500, 2200, 3100, 2200),          # sweep row 9, 3.00 bits
+        4: (2000, 800, 2400, 4800),           # sweep row 29, 4.00 bits
+        6: (0, 0, 0, 10000),
+    },
+    LEVELS_E: {
+        2: (3500, 2500, 4000),                # sweep row 52, 2.10 bits
+        3: (2500, 100, 7400),                 # sweep row 30, 2.98 bits
+        4: (0, 0, 10000),                     # sweep row 1
     },
 }
 

@@ -59,7 +59,9 @@ def test_resolve_auto_fields(g):
     (dict(K=100, N=512, level_bits=(0, 8)), -1),
     (dict(K=128, N=512, level_bits=(0, 8), group=64), -2),
     (dict(K=128, N=512, level_bits=(2, 8)), -1),
-    (dict(K=128, N=512, level_bits=(0, 4, 6)), -1),
+    (dict(K=128, N=512, level_bits=(0, 2, 5)), -2),     # b_max must be 4, 6 or 8
+    (dict(K=128, N=512, level_bits=(0, 2, 3)), -2),
+    (dict(K=128, N=512, level_bits=(0, 4, 10)), -2),
     (dict(K=128, N=512, level_bits=(0, 4, 4, 8)), -1),
     (dict(K=128, N=512, level_bits=(0,)), -1),
     (dict(K=128, N=512, level_bits=(0, 3, 8), plane_bits=2), -1),
@@ -81,6 +83,11 @@ def test_packed_bytes_and_workspace(g):
     d = g.make_desc(4096, 14336, (0, 2, 4, 6, 8))
     assert g.grinqh_packed_bytes(d) == (4096 * 14336, 32 * 14336 * 2)
     assert g.grinqh_workspace_bytes(d, 4) == 0
+    # b_max = 6 and 4: rows of T*b_max/8 bytes (Sec. 3.3 stores 4, 6 or 8 bits)
+    assert g.grinqh_packed_bytes(g.make_desc(4096, 14336, (0, 2, 4, 6)))[0] == 4096 * 14336 * 6 // 8
+    assert g.grinqh_packed_bytes(g.make_desc(4096, 14336, (0, 2, 4)))[0] == 4096 * 14336 // 2
+    r = g.grinqh_resolve_desc(g.make_desc(1024, 1024, (0, 1, 2, 4)))
+    assert r.plane_bits == 1 and g.grinqh_packed_bytes(r)[0] == 1024 * 1024 // 2
 
 
 @pytest.mark.parametrize("K", [1, 7, 128, 1024, 4096, 14336])

@@ -48,22 +48,25 @@ class Layer:
     def __init__(self, g, torch, K, N, levels, cfg=50, layer=0, tile_n=0, codes_src=False):
         self.desc = g.grinqh_resolve_desc(g.make_desc(K, N, levels, tile_n=tile_n))
         self.levels = tuple(levels)
+        self.b_max = int(levels[-1])
         self.K, self.N = K, N
         if codes_src:
             self.codes = inputs.random_codes(N, K, cfg, layer)
+            if self.b_max < 8:
+                self.codes = (self.codes & ((1 << self.b_max) - 1)).astype(np.uint8)
             sc_nk = inputs.random_scales(N, K, 128, cfg, layer)
             self.scales = np.ascontiguousarray(sc_nk.T)
             self.pc, self.ps = g.grinqh_pack(self.desc, codes=_dev(torch, self.codes),
                                              scales=_dev(torch, sc_nk))
         else:
             W = inputs.weights(N, K, cfg, layer)
-            self.codes, self.scales = orc.rtn_quantize(W)
+            self.codes, self.scales = orc.rtn_quantize(W, b_max=self.b_max)
             self.pc, self.ps = g.grinqh_pack(self.desc, W=_dev(torch, W))
         torch.cuda.synchronize()
 
     def check_packed(self):
         u, T = self.desc.plane_bits, self.desc.tile_n
-        want = orc.pack_codes_fast(self.codes, u, T)
+        want = orc.pack_codes_fast(self.codes, u, T, self.b_max)
         got = _host(self.pc)
         assert np.array_equal(got, want), f"packed codes differ at {np.nonzero(got != want)[0][:8]}"
         assert np.array_equal(_host(self.ps).view(np.uint16), self.scales.view(np.uint16))
@@ -505,3 +508,73 @@ def test_prefill_tile_configs(g, torch, tile, K, N, levels, tile_n, M, monkeypat
     y = _host(g.grinqh_prefill(L.desc, L.pc, L.ps, _dev(torch, x)))
     assert normwise(y, orc.prefill(L.codes, L.scales, x)) <= TOL
     assert prefill_bound_ok(y, L.codes, L.scales, x)
+
+
+
+# ------------------------------------------------ b_max = 4 and 6 storage ----
+# Sec. 3.3 stores the codes at b_max in {4, 6, 8} bits; the top level reads
+# all of them.  Every entry point runs on the narrower rows.
+BMAX_LEVELS = [(0, 2, 4), (0, 2, 4, 6), (0, 1, 2, 3, 4), (0, 2, 3, 4, 6)]
+
+
+@pytest.mark.parametrize("levels", BMAX_LEVELS)
+@pytest.mark.parametrize("codes_src", [False, True])
+def test_pack_bmax_bit_exact(g, torch, levels, codes_src):
+    for tile_n in (0, 512, 1024):
+        L = Layer(g, torch, 384, 2048, levels, cfg=80, layer=tile_n, tile_n=tile_n, codes_src=codes_src)
+        assert L.desc.plane_bits == orc.plane_bits_for(levels)
+        assert L.pc.numel() == 384 * 2048 * L.b_max // 8
+        L.check_packed()
+
+
+@pytest.mark.parametrize("levels", BMAX_LEVELS)
+@pytest.mark.parametrize("kernel", ["auto", "dot2", "v0"])
+def test_vmm_bmax_random_level_maps(g, torch, levels, kernel, monkeypatch):
+    if kernel != "auto":
+        monkeypatch.setenv("GRINQH_VMM_KERNEL", kernel)
+    if kernel == "dot2" and orc.plane_bits_for(levels) == 1:
+        pytest.skip("the per-plane kernels read 2-bit planes")
+    K, N = 1152, 1024
+    L = Layer(g, torch, K, N, levels, cfg=81, codes_src=True)
+    rng = np.random.default_rng(81)
+    for B in (1, 2, 4):
+        x = inputs.activations_t3(K, B, 81, B)
+        lm = rng.integers(0, len(levels), size=(B, K)).astype(np.uint8)
+        y, ref = _vmm_case(g, torch, L, x, lm)
+        assert normwise(y, ref) <= TOL, (B, normwise(y, ref))
+    # every channel at the top level is the plain dequantised matvec at b_max
+    x = inputs.activations_t3(K, 1, 81, 9)
+    top = np.full((1, K), len(levels) - 1, dtype=np.uint8)
+    y, ref = _vmm_case(g, torch, L, x, top)
+    assert normwise(y, ref) <= TOL
+
+
+@pytest.mark.parametrize("levels", [(0, 2, 4), (0, 2, 4, 6)])
+def test_vmm_bmax_topk_and_threshold(g, torch, levels):
+    K, N = 4096, 4096
+    L = Layer(g, torch, K, N, levels, cfg=82)
+    x = inputs.activations_t3(K, 2, 82, 1)
+    for p in inputs.BUDGETS[tuple(levels)].values():
+        counts = g.grinqh_topk_counts(K, p)
+        lm = _host(g.grinqh_assign(L.desc, _dev(torch, x), g.GRINQH_ASSIGN_TOPK, counts=counts))
+        y, ref = _vmm_case(g, torch, L, x, lm)
+        assert normwise(y, ref) <= TOL, p
+    th = np.sort(np.abs(x[0].astype(np.float32)))[[1000, 2000, 3000][:len(levels) - 1]]
+    lm_out = torch.zeros((2, K), dtype=torch.uint8, device="cuda")
+    y = g.grinqh_vmm_threshold(L.desc, L.pc, L.ps, _dev(torch, x), th, level_map_out=lm_out)
+    torch.cuda.synchronize()
+    lm = orc.assign_threshold(x, th)
+    assert np.array_equal(_host(lm_out), lm)
+    assert normwise(_host(y), orc.vmm_batch(L.codes, L.scales, x, lm, levels)) <= TOL
+
+
+@pytest.mark.parametrize("levels", BMAX_LEVELS)
+@pytest.mark.parametrize("tile", ["0", "1", "2"])
+def test_prefill_bmax(g, torch, levels, tile, monkeypatch):
+    monkeypatch.setenv("GRINQH_PREFILL_TILE", tile)
+    K, N, M = 384, 1024, 200
+    L = Layer(g, torch, K, N, levels, cfg=83, layer=int(tile), tile_n=512)
+    x = inputs.activations_t3(K, M, 83, int(tile))
+    y = _host(g.grinqh_prefill(L.desc, L.pc, L.ps, _dev(torch, x)))
+    ref = orc.prefill(L.codes, L.scales, x, b_max=L.b_max)
+    assert normwise(y, ref) <= TOL
