@@ -225,6 +225,38 @@ def prefill(codes, scales, x16, group: int = 128, b_max: int = B_MAX) -> np.ndar
     return X @ W.T
 
 
+def vmm_lut(codes, luts, x16, levels, level_bits) -> np.ndarray:
+    """Non-uniform nested weights read through look-up tables (Sec. 3.3: the
+    format only needs the nested property, which k-means-style nested weights
+    have; their levels are centred, so there is no phi; App. "Evaluation of
+    Nested Weight Formats").  luts[b] is an fp16 [N, 2^b] table per level
+    width b; a channel at level l (b = level_bits[l] > 0) reads the b most
+    significant bits q_b of the b_max-bit code and weighs x_k by
+    luts[b][n][q_b]; level 0 is skipped.  One token: float64 [N]."""
+    b_max = int(level_bits[-1])
+    codes = np.asarray(codes).astype(np.int64)
+    N, K = codes.shape
+    x = np.asarray(x16, dtype=np.float16).astype(np.float64).reshape(-1)
+    levels = np.asarray(levels).reshape(K)
+    W = np.zeros((N, K), dtype=np.float64)
+    rows = np.arange(N)[:, None]
+    for lvl, b in enumerate(level_bits):
+        b = int(b)
+        cols = np.nonzero(levels == lvl)[0]
+        if cols.size == 0 or b == 0:
+            continue
+        qb = nested_code(codes[:, cols], b, b_max)                  # [N, |cols|]
+        W[:, cols] = np.asarray(luts[b], dtype=np.float16).astype(np.float64)[rows, qb]
+    return W @ x
+
+
+def vmm_lut_batch(codes, luts, x16, levels, level_bits) -> np.ndarray:
+    """Tokens are independent (float64 [B, N])."""
+    x16 = np.atleast_2d(np.asarray(x16, dtype=np.float16))
+    levels = np.atleast_2d(np.asarray(levels))
+    return np.stack([vmm_lut(codes, luts, x16[t], levels[t], level_bits) for t in range(x16.shape[0])])
+
+
 # ---------------------------------------------------------------------------
 # 6. Packed nested layout (Sec. 3.3 and App. C.1, as re-laid-out for CDNA4)
 # ---------------------------------------------------------------------------

@@ -83,6 +83,25 @@ def activations_swiglu(K: int, tokens: int, config: int = 1, layer: int = 0, see
     return (silu * uu).astype(np.float16)
 
 
+def nested_luts(N: int, level_bits, config: int = 1, layer: int = 0, seed: int = 0):
+    """Synthetic per-output nested look-up tables, shaped like any-precision
+    (nested k-means) weights: for every output n, 2^b_max sorted centroids of
+    a N(0, 0.02) row at the top width b_max = level_bits[-1]; the table of a
+    narrower width b holds, for each b-bit prefix c, the mean of the
+    2^(b_max-b) centroids under it.  Returns {b: fp16 [N, 2^b]} for every
+    b > 0 in level_bits."""
+    b_max = int(level_bits[-1])
+    g = rng(config, layer, ROLE_CODES, seed + 2)
+    top = np.sort(g.normal(0.0, 0.02, size=(N, 2 ** b_max)), axis=1)
+    out = {}
+    for b in level_bits:
+        b = int(b)
+        if b == 0:
+            continue
+        out[b] = top.reshape(N, 2 ** b, 2 ** (b_max - b)).mean(axis=2).astype(np.float16)
+    return out
+
+
 # --------------------------------------------------------------------------
 # Level sets and precision distributions (basis points, sum 10000).
 # The {0,2,4,6,8} rows marked "sweep" are rows of the paper's precision
