@@ -101,7 +101,8 @@ GRINQH_API int grinqh_packed_bytes(const grinqh_layer_desc* desc, size_t* codes_
  *   src_kind GRINQH_SRC_CODES_U8: src = uint8 codes q[N][K] (q < 2^b_max;
  *     higher bits are ignored) from any base quantiser with the same
  *     offset-binary convention, src_scales = fp16 s[N][K/128] (the method is
- *     quantisation-agnostic, Sec. 3.3).
+ *     quantisation-agnostic, Sec. 3.3).  Codes of the look-up-table format
+ *     (grinqh_vmm_lut) have no scales: pass src_scales = packed_scales = NULL.
  *   Outputs: packed_codes (K*N*b_max/8 bytes, layout above), packed_scales
  *   (fp16 [K/128][N]).  Inputs and outputs must not overlap. */
 GRINQH_API int grinqh_pack(const grinqh_layer_desc* desc, int src_kind, const void* src,
@@ -193,6 +194,28 @@ GRINQH_API int grinqh_vmm_threshold(const grinqh_layer_desc* desc, const void* p
 GRINQH_API int grinqh_prefill(const grinqh_layer_desc* desc, const void* packed_codes,
                               const void* packed_scales, const void* x, int32_t M, float* y,
                               int32_t flags, void* stream);
+
+/* Number of fp16 table entries of a layer's look-up tables (host only):
+ * N * sum over levels l >= 1 of 2^b_l. */
+GRINQH_API int grinqh_lut_entries(const grinqh_layer_desc* desc, size_t* entries);
+
+/* Decode VMM over non-uniform nested weights read through look-up tables
+ * (Sec. 3.3: any quantiser with the nested property, e.g. nested k-means
+ * weights, whose levels are centred so no midpoint bias applies; appendix
+ * on nested weight formats).  Codes are packed as for grinqh_vmm (codes
+ * source, no scales).
+ *   luts: fp16, for each level l = 1..n (b = b_l bits) a table [N][2^b],
+ *   the tables consecutive in level order: level l's table starts at
+ *   element N * sum_{1 <= i < l} 2^b_i (16-byte aligned base).
+ *   y[t][n] = sum_k x[t][k] * luts_l[n][q_b], l = level_map[t][k] (a value
+ *   >= n_levels is read as the top level), q_b = the b leading bits of the
+ *   b_max-bit code; level 0 skipped.
+ *   x: fp16 [B][K]; level_map: uint8 [B][K]; y: fp32 [B][N]; 1 <= B <= 65535.
+ *   flags: 0 -> y is overwritten; GRINQH_VMM_ACCUMULATE -> y += result.
+ *   Partial sums meet in atomics: reproducible to rounding, not bit for bit. */
+GRINQH_API int grinqh_vmm_lut(const grinqh_layer_desc* desc, const void* packed_codes,
+                              const void* luts, const void* x, const uint8_t* level_map,
+                              int32_t B, float* y, int32_t flags, void* stream);
 
 /* Message of the last failing call on this thread ("" if none). */
 GRINQH_API const char* grinqh_last_error(void);

@@ -11,7 +11,7 @@ CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libgrinqh.so")
 SOURCES = ["grinqh_api.hip", "pack.hip", "assign.hip", "vmm.hip", "vmm_dot2.hip", "vmm_pp.hip",
-           "prefill.hip"]
+           "prefill.hip", "vmm_lut.hip"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",

@@ -139,9 +139,11 @@ int grinqh_pack(const grinqh_layer_desc* desc, int src_kind, const void* src, co
   if (st) return st;
   if (src_kind != GRINQH_SRC_FP16_RTN && src_kind != GRINQH_SRC_CODES_U8)
     return fail(GRINQH_EINVAL, "src_kind=%d is not a known source kind", src_kind);
-  if (!src || !packed_codes || !packed_scales) return fail(GRINQH_EINVAL, "src and packed buffers must not be NULL");
-  if (src_kind == GRINQH_SRC_CODES_U8 && !src_scales) return fail(GRINQH_EINVAL, "src_scales is NULL for a codes source");
+  if (!src || !packed_codes) return fail(GRINQH_EINVAL, "src and packed_codes must not be NULL");
   if (src_kind == GRINQH_SRC_FP16_RTN && src_scales) return fail(GRINQH_EINVAL, "src_scales must be NULL for an fp16 source");
+  if (src_kind == GRINQH_SRC_FP16_RTN && !packed_scales) return fail(GRINQH_EINVAL, "packed_scales is NULL for an fp16 source");
+  if (src_kind == GRINQH_SRC_CODES_U8 && (!src_scales) != (!packed_scales))
+    return fail(GRINQH_EINVAL, "a codes source takes src_scales and packed_scales together, or neither");
   return launch_pack(L, src_kind, src, src_scales, packed_codes, packed_scales, (hipStream_t)stream);
 }
 
@@ -312,6 +314,36 @@ int grinqh_prefill(const grinqh_layer_desc* desc, const void* packed_codes,
     return fail(GRINQH_EINVAL, "packed codes, scales and x must be 16-byte aligned");
   if ((uintptr_t)y & 3u) return fail(GRINQH_EINVAL, "y must be 4-byte aligned");
   return launch_prefill(L, packed_codes, packed_scales, x, M, y, flags & GRINQH_VMM_ACCUMULATE,
+                        (hipStream_t)stream);
+}
+
+int grinqh_lut_entries(const grinqh_layer_desc* desc, size_t* entries) {
+  clear_error();
+  Layer L;
+  int st = resolve(desc, &L, nullptr);
+  if (st) return st;
+  if (!entries) return fail(GRINQH_EINVAL, "entries is NULL");
+  LutDesc D;
+  lut_desc(L, &D);
+  *entries = (size_t)L.N * (size_t)D.entries;
+  return GRINQH_OK;
+}
+
+int grinqh_vmm_lut(const grinqh_layer_desc* desc, const void* packed_codes, const void* luts,
+                   const void* x, const uint8_t* level_map, int32_t B, float* y, int32_t flags,
+                   void* stream) {
+  clear_error();
+  Layer L;
+  int st = resolve(desc, &L, nullptr);
+  if (st) return st;
+  if (!packed_codes || !luts || !x || !level_map || !y)
+    return fail(GRINQH_EINVAL, "codes, luts, x, level_map and y must not be NULL");
+  if (B < 1 || B > 65535) return fail(GRINQH_EINVAL, "B=%d outside 1..65535", B);
+  if (flags & ~GRINQH_VMM_ACCUMULATE) return fail(GRINQH_EINVAL, "unknown flags 0x%x", flags);
+  if (((uintptr_t)packed_codes | (uintptr_t)luts) & 15u)
+    return fail(GRINQH_EINVAL, "packed codes and luts must be 16-byte aligned");
+  if (((uintptr_t)x | (uintptr_t)y) & 3u) return fail(GRINQH_EINVAL, "x and y must be 4-byte aligned");
+  return launch_vmm_lut(L, packed_codes, luts, x, level_map, B, y, flags & GRINQH_VMM_ACCUMULATE,
                         (hipStream_t)stream);
 }
 

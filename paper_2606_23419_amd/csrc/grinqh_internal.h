@@ -49,6 +49,15 @@ struct QuantilePos {
   int n;
 };
 
+// Per-output look-up tables of the LUT VMM: level l's table [N][2^b_l]
+// starts at element offset[l] of the table array; cum[l] = sum of 2^b_i over
+// 1 <= i < l (the level's position within one output's entries).
+struct LutDesc {
+  long offset[kMaxLevels];
+  int cum[kMaxLevels];
+  int entries;      // sum over levels >= 1 of 2^b_l
+};
+
 struct TopkCuts {
   int cum[kMaxLevels];           // cum[j] = C_{j+1}: channels at level >= j+1
   int n;
@@ -88,5 +97,8 @@ int launch_vmm(const Layer& L, const void* codes, const void* scales, const void
                int B, float* y, int accumulate, hipStream_t s);
 int launch_prefill(const Layer& L, const void* codes, const void* scales, const void* x, int M,
                    float* y, int accumulate, hipStream_t s);
+int lut_desc(const Layer& L, LutDesc* D);
+int launch_vmm_lut(const Layer& L, const void* codes, const void* luts, const void* x,
+                   const uint8_t* level_map, int B, float* y, int accumulate, hipStream_t s);
 
 }  // namespace grinqh

@@ -106,7 +106,7 @@ int launch_pack(const Layer& L, int src_kind, const void* src, const void* src_s
     hipLaunchKernelGGL(k_rtn_scales, dim3((unsigned)blocks), dim3(256), 0, s,
                        (const uint16_t*)src, (uint16_t*)packed_scales, L.N, L.K,
                        (float)((1 << (L.bmax - 1)) - 1));
-  } else {
+  } else if (src_scales) {   // codes without scales: the look-up-table format
     const long n = (long)L.N * L.groups;
     hipLaunchKernelGGL(k_transpose_scales, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s,
                        (const uint16_t*)src_scales, (uint16_t*)packed_scales, L.N, L.groups);

@@ -1,0 +1,171 @@
+// Nested-precision decode VMM over non-uniform nested weights read through
+// per-output look-up tables (Sec. 3.3: the format needs only the nested
+// property, which k-means-style nested weights have; their levels are
+// centred, so no midpoint bias is applied).  The codes use the packed
+// layout of the uniform path; a channel at width b reads its first b/u
+// planes, forms the b leading bits q_b of every output's code, and adds
+// x_k * table_b[n][q_b].
+//
+// A workgroup owns 64 outputs of one tile (a sub-tile), a run of groups and
+// one token.  The tables of its 64 outputs, every level, are copied to LDS
+// once: for each level they are one contiguous block of the table array.
+// 4 lanes cover a channel row's 64 outputs (16 each); the 64 row slots of
+// the workgroup take two rows of each group.  Every weight is one LDS
+// lookup.  Lanes holding the same outputs are reduced with shuffles, waves
+// through LDS, and the sums added into y with atomics.
+#include <cstdlib>
+
+#include "grinqh_internal.h"
+
+namespace grinqh {
+
+namespace {
+
+constexpr int kLutThreads = 256;
+constexpr int kSub = 64;                     // outputs per workgroup
+
+__global__ __launch_bounds__(kLutThreads) void k_zero_lut(float* __restrict__ y, long n) {
+  const long i = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) y[i] = 0.0f;
+}
+
+template <int U>
+__global__ __launch_bounds__(kLutThreads) void k_vmm_lut(const uint8_t* __restrict__ codes,
+                                                        const uint16_t* __restrict__ luts,
+                                                        const uint16_t* __restrict__ x,
+                                                        const uint8_t* __restrict__ lm,
+                                                        float* __restrict__ y, Layer L, LutDesc D,
+                                                        int groups_per_split) {
+  constexpr uint32_t MASK = (1u << U) - 1u;
+  extern __shared__ __align__(16) uint16_t s_lut[];          // [levels][kSub][2^b]
+  __shared__ float s_red[kLutThreads / 64][kSub];
+  __shared__ int s_cum[kMaxLevels];                           // level l's block starts at kSub * s_cum[l]
+
+  const int subs = L.T / kSub;
+  const int tile_sub = blockIdx.x % (L.tiles * subs);
+  const int split = blockIdx.x / (L.tiles * subs);
+  const int t = tile_sub / subs, sub = tile_sub % subs;
+  const int tok = blockIdx.y;
+  const int n0 = t * L.T + sub * kSub;       // first output of the sub-tile
+  const int g0 = split * groups_per_split;
+  const int g1 = min(g0 + groups_per_split, L.groups);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+
+  if (tid < kMaxLevels) s_cum[tid] = D.cum[tid];
+  // tables of the 64 outputs: level l's block is kSub * 2^b entries at
+  // D.offset[l] + n0 * 2^b of the table array, copied in 16-byte pieces
+  for (int l = 1; l < L.n_levels; ++l) {
+    const int e = 1 << L.bits[l];
+    const uint4* src = (const uint4*)(luts + D.offset[l] + (size_t)n0 * e);
+    uint4* dst = (uint4*)(s_lut + kSub * D.cum[l]);
+    for (int i = tid; i < kSub * e / 8; i += kLutThreads) dst[i] = src[i];
+  }
+  __syncthreads();
+
+  const int c = tid & 3;                     // outputs 16 c .. 16 c + 15 of the sub-tile
+  const int rs = tid >> 2;                   // row slot: rows rs and rs + 64 of each group
+  const int plane_bytes = L.T * U / 8;
+  const int col = (sub * kSub + 16 * c) * U / 8;   // byte of the lane's outputs in a plane row
+  const uint16_t* xt = x + (size_t)tok * L.K;
+  const uint8_t* lmt = lm + (size_t)tok * L.K;
+  const int n_top = L.n_levels - 1;
+
+  float acc[16];
+#pragma unroll
+  for (int e = 0; e < 16; ++e) acc[e] = 0.0f;
+
+  for (int g = g0; g < g1; ++g) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int k = g * kGroup + rs + 64 * h;
+      const int lvl = min((int)lmt[k], n_top);
+      if (lvl == 0) continue;
+      const float xv = h2f(xt[k]);
+      const int d = level_planes(L.planes_packed, lvl);
+      const int b = d * U;
+      const uint8_t* row = codes + ((size_t)t * L.K + k) * L.RB + col;
+      uint32_t q[16];
+#pragma unroll
+      for (int e = 0; e < 16; ++e) q[e] = 0u;
+      for (int j = 0; j < d; ++j) {
+        uint32_t word;
+        if constexpr (U == 2) word = *(const uint32_t*)(row + (size_t)j * plane_bytes);
+        else word = *(const uint16_t*)(row + (size_t)j * plane_bytes);
+#pragma unroll
+        for (int e = 0; e < 16; ++e) q[e] = (q[e] << U) | ((word >> (e * U)) & MASK);
+      }
+      // the lane's outputs' rows of level lvl's table: output 16 c + e at
+      // (16 c + e) * 2^b, q_b = q[e] below it
+      const uint16_t* tb = s_lut + kSub * s_cum[lvl] + ((16 * c) << b);
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[e] = fmaf(xv, h2f(tb[(e << b) + q[e]]), acc[e]);
+    }
+  }
+
+  // lanes with equal (lane & 3) hold the same outputs: sum over lane bits 2..5
+#pragma unroll
+  for (int e = 0; e < 16; ++e) {
+#pragma unroll
+    for (int m = 4; m < 64; m <<= 1) acc[e] += __shfl_xor(acc[e], m);
+  }
+  if (lane < 4) {
+#pragma unroll
+    for (int e = 0; e < 16; ++e) s_red[wave][16 * lane + e] = acc[e];
+  }
+  __syncthreads();
+  if (tid < kSub) {
+    float v = 0.0f;
+#pragma unroll
+    for (int w = 0; w < kLutThreads / 64; ++w) v += s_red[w][tid];
+    atomicAdd(&y[(size_t)tok * L.N + n0 + tid], v);
+  }
+}
+
+}  // namespace
+
+int lut_desc(const Layer& L, LutDesc* D) {
+  long off = 0;
+  int cum = 0;
+  for (int l = 0; l < kMaxLevels; ++l) {
+    D->offset[l] = off;
+    D->cum[l] = cum;
+    if (l >= 1 && l < L.n_levels) {
+      off += (long)L.N << L.bits[l];
+      cum += 1 << L.bits[l];
+    }
+  }
+  D->entries = cum;
+  return GRINQH_OK;
+}
+
+int launch_vmm_lut(const Layer& L, const void* codes, const void* luts, const void* x,
+                   const uint8_t* level_map, int B, float* y, int accumulate, hipStream_t s) {
+  LutDesc D;
+  lut_desc(L, &D);
+  const size_t lds = (size_t)kSub * D.entries * 2;   // <= 64 * 510 * 2 bytes: levels are distinct widths <= 8
+  if (lds > 65536) return fail(GRINQH_EUNSUPPORTED, "LUT VMM: %d table entries per output", D.entries);
+  if (!accumulate) {
+    const long n = (long)B * L.N;
+    hipLaunchKernelGGL(k_zero_lut, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, y, n);
+  }
+  // about two workgroups per CU over (sub-tiles x K splits x tokens)
+  const long subtiles = (long)L.tiles * (L.T / kSub);
+  long splits = (512 + subtiles * B - 1) / (subtiles * B);
+  splits = splits < 1 ? 1 : (splits > L.groups ? L.groups : splits);
+  int gps = (int)((L.groups + splits - 1) / splits);
+  if (const char* e = getenv("GRINQH_LUT_GPS")) {
+    const int v = atoi(e);
+    if (v >= 1 && v <= L.groups) gps = v;
+  }
+  splits = (L.groups + gps - 1) / gps;
+  const dim3 grid((unsigned)(subtiles * splits), (unsigned)B);
+  if (L.u == 2)
+    hipLaunchKernelGGL(k_vmm_lut<2>, grid, dim3(kLutThreads), lds, s, (const uint8_t*)codes,
+                       (const uint16_t*)luts, (const uint16_t*)x, level_map, y, L, D, gps);
+  else
+    hipLaunchKernelGGL(k_vmm_lut<1>, grid, dim3(kLutThreads), lds, s, (const uint8_t*)codes,
+                       (const uint16_t*)luts, (const uint16_t*)x, level_map, y, L, D, gps);
+  return check_launch("vmm_lut");
+}
+
+}  // namespace grinqh

@@ -30,7 +30,8 @@ MAX_LEVELS = 9
 EXPORTED = (
     "grinqh_resolve_desc", "grinqh_packed_bytes", "grinqh_pack", "grinqh_topk_counts",
     "grinqh_workspace_bytes", "grinqh_calibrate", "grinqh_assign", "grinqh_vmm",
-    "grinqh_vmm_threshold", "grinqh_prefill", "grinqh_last_error",
+    "grinqh_vmm_threshold", "grinqh_prefill", "grinqh_lut_entries", "grinqh_vmm_lut",
+    "grinqh_last_error",
 )
 
 
@@ -76,6 +77,8 @@ def _load():
         "grinqh_vmm_threshold": [dp, vp, vp, vp, i32, ctypes.POINTER(ctypes.c_float), vp, vp,
                                  i32, vp, sz, vp],
         "grinqh_prefill": [dp, vp, vp, vp, i32, vp, i32, vp],
+        "grinqh_lut_entries": [dp, ctypes.POINTER(sz)],
+        "grinqh_vmm_lut": [dp, vp, vp, vp, vp, i32, vp, i32, vp],
     }
     for name, args in sig.items():
         f = getattr(lib, name)
@@ -187,9 +190,9 @@ def grinqh_pack(desc: LayerDesc, W=None, codes=None, scales=None, out_codes=None
                              _stream(stream))
     else:
         src = _dev(codes, torch.uint8, "codes", (rd.N, rd.K))
-        sc = _dev(scales, torch.float16, "scales", (rd.N, rd.K // 128))
-        st = lib.grinqh_pack(ctypes.byref(rd), GRINQH_SRC_CODES_U8, src, sc, pc, ps,
-                             _stream(stream))
+        sc = _dev(scales, torch.float16, "scales", (rd.N, rd.K // 128)) if scales is not None else None
+        st = lib.grinqh_pack(ctypes.byref(rd), GRINQH_SRC_CODES_U8, src, sc, pc,
+                             ps if scales is not None else None, _stream(stream))
     _check(st)
     return out_codes, out_scales
 
@@ -300,4 +303,45 @@ def grinqh_prefill(desc: LayerDesc, packed_codes, packed_scales, x, y=None,
     yp = _dev(y, torch.float32, "y", (M, rd.N))
     flags = GRINQH_VMM_ACCUMULATE if accumulate else 0
     _check(lib.grinqh_prefill(ctypes.byref(rd), cp, sp, xp, M, yp, flags, _stream(stream)))
+    return y
+
+
+def grinqh_lut_entries(desc: LayerDesc) -> int:
+    n = ctypes.c_size_t()
+    _check(lib.grinqh_lut_entries(ctypes.byref(desc), ctypes.byref(n)))
+    return n.value
+
+
+def lut_table_array(desc: LayerDesc, tables, device=None):
+    """Concatenate per-level fp16 tables {b: [N, 2^b]} in level order into
+    the 1-D table array of grinqh_vmm_lut (host-side layout helper)."""
+    torch = _torch()
+    rd = grinqh_resolve_desc(desc)
+    parts = [torch.as_tensor(tables[int(rd.level_bits[l])]).reshape(-1)
+             for l in range(1, rd.n_levels)]
+    out = torch.cat(parts).to(torch.float16)
+    assert out.numel() == grinqh_lut_entries(rd)
+    return out.to(device) if device is not None else out
+
+
+def grinqh_vmm_lut(desc: LayerDesc, packed_codes, luts, x, level_map, y=None,
+                   accumulate: bool = False, stream=None):
+    """y fp32 [B, N] of the look-up-table nested VMM (see grinqh.h)."""
+    torch = _torch()
+    rd = grinqh_resolve_desc(desc)
+    if x.dim() == 1:
+        x = x.view(1, -1)
+    if level_map.dim() == 1:
+        level_map = level_map.view(1, -1)
+    B = int(x.shape[0])
+    cp = _dev(packed_codes, torch.uint8, "packed_codes",
+              (rd.K * rd.N * rd.level_bits[rd.n_levels - 1] // 8,))
+    lp = _dev(luts, torch.float16, "luts", (grinqh_lut_entries(rd),))
+    xp = _dev(x, torch.float16, "x", (B, rd.K))
+    mp = _dev(level_map, torch.uint8, "level_map", (B, rd.K))
+    if y is None:
+        y = torch.empty((B, rd.N), dtype=torch.float32, device=x.device)
+    yp = _dev(y, torch.float32, "y", (B, rd.N))
+    flags = GRINQH_VMM_ACCUMULATE if accumulate else 0
+    _check(lib.grinqh_vmm_lut(ctypes.byref(rd), cp, lp, xp, mp, B, yp, flags, _stream(stream)))
     return y

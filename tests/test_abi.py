@@ -116,7 +116,9 @@ def test_pack_validation(g):
     assert _call_pack(g, d, 7, FAKE, None, FAKE, FAKE) == -1
     assert _call_pack(g, d, 0, None, None, FAKE, FAKE) == -1
     assert _call_pack(g, d, 0, FAKE, FAKE, FAKE, FAKE) == -1       # scales given for fp16
-    assert _call_pack(g, d, 1, FAKE, None, FAKE, FAKE) == -1       # scales missing for codes
+    assert _call_pack(g, d, 1, FAKE, None, FAKE, FAKE) == -1       # scales in but not out
+    assert _call_pack(g, d, 1, FAKE, FAKE, FAKE, None) == -1       # scales out but not in
+    assert _call_pack(g, d, 0, FAKE, None, FAKE, None) == -1       # fp16 source needs scales out
     bad = g.make_desc(250, 512, (0, 2, 4, 8))
     assert _call_pack(g, bad, 0, FAKE, None, FAKE, FAKE) == -1
 
@@ -192,6 +194,21 @@ def test_prefill_validation(g):
     assert P(ctypes.byref(d), FAKE, FAKE, FAKE, 1, ctypes.c_void_p(0x1002), 0, None) == -1
     bad = g.make_desc(200, 512, (0, 8))
     assert P(ctypes.byref(bad), FAKE, FAKE, FAKE, 1, FAKE, 0, None) == -1
+
+
+def test_lut_entries_and_validation(g):
+    # one fp16 table of 2^b entries per output and level above 0
+    assert g.grinqh_lut_entries(g.make_desc(1024, 512, (0, 2, 4, 6, 8))) == 512 * (4 + 16 + 64 + 256)
+    assert g.grinqh_lut_entries(g.make_desc(1024, 512, (0, 2, 4))) == 512 * 20
+    assert g.grinqh_lut_entries(g.make_desc(1024, 1024, (0, 1, 2, 3, 4, 5, 6, 7, 8))) == 1024 * 510
+    d = g.make_desc(256, 512, (0, 2, 4, 8))
+    V = g.lib.grinqh_vmm_lut
+    assert V(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, 0, FAKE, 0, None) == -1
+    assert V(ctypes.byref(d), FAKE, None, FAKE, FAKE, 1, FAKE, 0, None) == -1
+    assert V(ctypes.byref(d), FAKE, FAKE, FAKE, None, 1, FAKE, 0, None) == -1
+    assert V(ctypes.byref(d), FAKE, ctypes.c_void_p(0x1008), FAKE, FAKE, 1, FAKE, 0, None) == -1
+    assert V(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, 1, FAKE, 8, None) == -1
+    assert g.grinqh_last_error()
 
 
 def test_binding_rejects_host_tensors(g):

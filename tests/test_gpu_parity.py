@@ -578,3 +578,101 @@ def test_prefill_bmax(g, torch, levels, tile, monkeypatch):
     y = _host(g.grinqh_prefill(L.desc, L.pc, L.ps, _dev(torch, x)))
     ref = orc.prefill(L.codes, L.scales, x, b_max=L.b_max)
     assert normwise(y, ref) <= TOL
+
+
+# ------------------------------------------ look-up-table nested weights ----
+class LutLayer:
+    """Packed codes (no scales) and per-output nested tables of one layer."""
+
+    def __init__(self, g, torch, K, N, levels, cfg=90, layer=0, tile_n=0, tables=None):
+        self.desc = g.grinqh_resolve_desc(g.make_desc(K, N, levels, tile_n=tile_n))
+        self.levels = tuple(levels)
+        b_max = int(levels[-1])
+        self.codes = inputs.random_codes(N, K, cfg, layer)
+        if b_max < 8:
+            self.codes = (self.codes & ((1 << b_max) - 1)).astype(np.uint8)
+        self.tables = tables if tables is not None else inputs.nested_luts(N, levels, cfg, layer)
+        self.pc, _ = g.grinqh_pack(self.desc, codes=_dev(torch, self.codes))
+        self.luts = g.lut_table_array(self.desc, self.tables, device="cuda")
+        torch.cuda.synchronize()
+
+    def run(self, g, torch, x, lm, **kw):
+        y = g.grinqh_vmm_lut(self.desc, self.pc, self.luts, _dev(torch, x), _dev(torch, lm), **kw)
+        torch.cuda.synchronize()
+        return _host(y)
+
+    def ref(self, x, lm):
+        return orc.vmm_lut_batch(self.codes, self.tables, x, lm, self.levels)
+
+
+LUT_CASES = [  # K, N, levels, tile_n
+    (1152, 1024, (0, 2, 4, 8), 256),
+    (1152, 1024, (0, 2, 4, 6, 8), 512),
+    (640, 2048, (0, 2, 4, 6), 1024),
+    (384, 2048, (0, 2, 4), 2048),
+    (640, 1024, (0, 1, 2, 3, 4), 512),
+    (512, 2048, (0, 2, 3, 4, 8), 1024),
+]
+
+
+@pytest.mark.parametrize("K,N,levels,tile_n", LUT_CASES)
+def test_vmm_lut_parity(g, torch, K, N, levels, tile_n):
+    L = LutLayer(g, torch, K, N, levels, layer=K + N, tile_n=tile_n)
+    rng = np.random.default_rng(K + N)
+    for B in (1, 3):
+        x = inputs.activations_t3(K, B, 90, B)
+        lm = rng.integers(0, len(levels), size=(B, K)).astype(np.uint8)
+        assert normwise(L.run(g, torch, x, lm), L.ref(x, lm)) <= TOL, B
+    x = inputs.activations_t3(K, 1, 90, 7)
+    top = np.full((1, K), len(levels) - 1, dtype=np.uint8)
+    assert normwise(L.run(g, torch, x, top), L.ref(x, top)) <= TOL
+    assert np.all(L.run(g, torch, x, np.zeros((1, K), dtype=np.uint8)) == 0.0)
+
+
+@pytest.mark.parametrize("levels", [(0, 2, 4, 8), (0, 2, 4, 6)])
+def test_vmm_lut_with_uniform_tables_is_the_uniform_vmm(g, torch, levels):
+    # tables holding the uniform reconstruction (one power-of-two scale per
+    # output, exact in fp16) make the two GPU paths compute the same thing
+    K, N = 1024, 1024
+    b_max = levels[-1]
+    rng = np.random.default_rng(91)
+    s_out = 2.0 ** rng.integers(-9, -5, size=N).astype(np.float64)
+    tables = {}
+    for b in levels[1:]:
+        c = np.arange(2 ** b, dtype=np.float64)
+        vals = c * 2 ** (b_max - b) + orc.midpoint_bias(b, b_max) - 2 ** (b_max - 1)
+        tables[b] = (s_out[:, None] * vals[None, :]).astype(np.float16)
+    L = LutLayer(g, torch, K, N, levels, layer=3, tables=tables)
+    sc_nk = np.repeat(s_out[:, None], K // 128, axis=1).astype(np.float16)
+    pc, ps = g.grinqh_pack(L.desc, codes=_dev(torch, L.codes), scales=_dev(torch, sc_nk))
+    x = inputs.activations_t3(K, 2, 91, 0)
+    lm = rng.integers(0, len(levels), size=(2, K)).astype(np.uint8)
+    y_lut = L.run(g, torch, x, lm)
+    y_uni = _host(g.grinqh_vmm(L.desc, pc, ps, _dev(torch, x), _dev(torch, lm)))
+    assert normwise(y_lut, y_uni) <= 1e-5
+    assert normwise(y_lut, orc.vmm_batch(L.codes, np.ascontiguousarray(sc_nk.T), x, lm, levels)) <= TOL
+
+
+@pytest.mark.parametrize("gps", ["1", "3", "32"])
+def test_vmm_lut_full_size_topk(g, torch, gps, monkeypatch):
+    monkeypatch.setenv("GRINQH_LUT_GPS", gps)
+    K, N, levels = 4096, 4096, inputs.LEVELS_B
+    L = LutLayer(g, torch, K, N, levels, layer=4)
+    x = inputs.activations_t3(K, 1, 92, 0)
+    counts = g.grinqh_topk_counts(K, inputs.BUDGETS[levels][4])
+    lm = _host(g.grinqh_assign(L.desc, _dev(torch, x), g.GRINQH_ASSIGN_TOPK, counts=counts))
+    rows = np.sort(np.random.default_rng(92).choice(N, size=128, replace=False))
+    y = L.run(g, torch, x, lm)
+    ref = orc.vmm_lut_batch(L.codes[rows], {b: t[rows] for b, t in L.tables.items()}, x, lm, levels)
+    assert normwise(y[:, rows], ref) <= TOL
+
+
+def test_vmm_lut_accumulate(g, torch):
+    K, N, levels = 512, 1024, (0, 2, 4, 8)
+    L = LutLayer(g, torch, K, N, levels, layer=5)
+    x = inputs.activations_t3(K, 2, 93, 0)
+    lm = np.random.default_rng(93).integers(0, 4, size=(2, K)).astype(np.uint8)
+    base = np.random.default_rng(94).standard_normal((2, N)).astype(np.float32)
+    yd = _dev(torch, base)
+    L.run(g, torch, x, lm, y=yd, accumulate=True)
+    assert normwise(_host(yd), L.ref(x, lm) + base) <= TOL
