@@ -23,6 +23,7 @@ namespace {
 
 constexpr int kLutThreads = 256;
 constexpr int kSub = 64;                     // outputs per workgroup
+constexpr int kMaxRun = 16 * 128;            // channels per workgroup (16 groups)
 
 __global__ __launch_bounds__(kLutThreads) void k_zero_lut(float* __restrict__ y, long n) {
   const long i = (long)blockIdx.x * blockDim.x + threadIdx.x;
@@ -40,6 +41,8 @@ __global__ __launch_bounds__(kLutThreads) void k_vmm_lut(const uint8_t* __restri
   extern __shared__ __align__(16) uint16_t s_lut[];          // [levels][kSub][2^b]
   __shared__ float s_red[kLutThreads / 64][kSub];
   __shared__ int s_cum[kMaxLevels];                           // level l's block starts at kSub * s_cum[l]
+  __shared__ uint8_t s_lv[kMaxRun];                           // levels of the run's channels
+  __shared__ uint16_t s_x[kMaxRun];                           // x of the run's channels
 
   const int subs = L.T / kSub;
   const int tile_sub = blockIdx.x % (L.tiles * subs);
@@ -63,36 +66,58 @@ __global__ __launch_bounds__(kLutThreads) void k_vmm_lut(const uint8_t* __restri
   __syncthreads();
 
   const int c = tid & 3;                     // outputs 16 c .. 16 c + 15 of the sub-tile
-  const int rs = tid >> 2;                   // row slot: rows rs and rs + 64 of each group
+  const int rs = tid >> 2;                   // row slot: rows rs, rs + 64, ... of the run
   const int plane_bytes = L.T * U / 8;
   const int col = (sub * kSub + 16 * c) * U / 8;   // byte of the lane's outputs in a plane row
-  const uint16_t* xt = x + (size_t)tok * L.K;
-  const uint8_t* lmt = lm + (size_t)tok * L.K;
   const int n_top = L.n_levels - 1;
+  const int kr0 = g0 * kGroup, nrows = (g1 - g0) * kGroup;   // the workgroup's channels
+
+  // levels and x of the run's channels, staged once (<= kMaxRun channels)
+  for (int i = tid; i < nrows; i += kLutThreads) {
+    s_lv[i] = (uint8_t)min((int)lm[(size_t)tok * L.K + kr0 + i], n_top);
+    s_x[i] = x[(size_t)tok * L.K + kr0 + i];
+  }
+  __syncthreads();
 
   float acc[16];
 #pragma unroll
   for (int e = 0; e < 16; ++e) acc[e] = 0.0f;
 
-  for (int g = g0; g < g1; ++g) {
+  // rows rs + 64 m, m = 0, 1, ...: the plane words of the next row are
+  // requested before the current row's lookups
+  constexpr int kWords = 8 / U;
+  const uint8_t* tile_codes = codes + (size_t)t * L.K * L.RB + col;
+  auto fetch = [&](int i, uint32_t (&w)[kWords]) __attribute__((always_inline)) {
+    const int d = i < nrows ? level_planes(L.planes_packed, s_lv[i]) : 0;
+    const uint8_t* row = tile_codes + (size_t)(kr0 + min(i, nrows - 1)) * L.RB;
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      const int k = g * kGroup + rs + 64 * h;
-      const int lvl = min((int)lmt[k], n_top);
-      if (lvl == 0) continue;
-      const float xv = h2f(xt[k]);
+    for (int j = 0; j < kWords; ++j) {
+      if (j < d) {
+        if constexpr (U == 2) w[j] = *(const uint32_t*)(row + (size_t)j * plane_bytes);
+        else w[j] = *(const uint16_t*)(row + (size_t)j * plane_bytes);
+      } else {
+        w[j] = 0u;
+      }
+    }
+  };
+  uint32_t wa[kWords], wb[kWords];
+  fetch(rs, wa);
+  for (int i = rs; i < nrows; i += 64) {
+    fetch(i + 64, wb);
+    const int lvl = s_lv[i];
+    if (lvl != 0) {
+      const float xv = h2f(s_x[i]);
       const int d = level_planes(L.planes_packed, lvl);
       const int b = d * U;
-      const uint8_t* row = codes + ((size_t)t * L.K + k) * L.RB + col;
       uint32_t q[16];
 #pragma unroll
       for (int e = 0; e < 16; ++e) q[e] = 0u;
-      for (int j = 0; j < d; ++j) {
-        uint32_t word;
-        if constexpr (U == 2) word = *(const uint32_t*)(row + (size_t)j * plane_bytes);
-        else word = *(const uint16_t*)(row + (size_t)j * plane_bytes);
 #pragma unroll
-        for (int e = 0; e < 16; ++e) q[e] = (q[e] << U) | ((word >> (e * U)) & MASK);
+      for (int j = 0; j < kWords; ++j) {
+        if (j < d) {
+#pragma unroll
+          for (int e = 0; e < 16; ++e) q[e] = (q[e] << U) | ((wa[j] >> (e * U)) & MASK);
+        }
       }
       // the lane's outputs' rows of level lvl's table: output 16 c + e at
       // (16 c + e) * 2^b, q_b = q[e] below it
@@ -100,6 +125,8 @@ __global__ __launch_bounds__(kLutThreads) void k_vmm_lut(const uint8_t* __restri
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[e] = fmaf(xv, h2f(tb[(e << b) + q[e]]), acc[e]);
     }
+#pragma unroll
+    for (int j = 0; j < kWords; ++j) wa[j] = wb[j];
   }
 
   // lanes with equal (lane & 3) hold the same outputs: sum over lane bits 2..5
@@ -157,6 +184,7 @@ int launch_vmm_lut(const Layer& L, const void* codes, const void* luts, const vo
     const int v = atoi(e);
     if (v >= 1 && v <= L.groups) gps = v;
   }
+  gps = gps > kMaxRun / kGroup ? kMaxRun / kGroup : gps;
   splits = (L.groups + gps - 1) / gps;
   const dim3 grid((unsigned)(subtiles * splits), (unsigned)B);
   if (L.u == 2)
