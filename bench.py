@@ -411,6 +411,9 @@ def run_lut(args, torch, g, wl_name, wl):
     ys = {name: torch.zeros((T, N), dtype=torch.float32, device=dev) for name, _, N, _, _ in layers}
 
     def step(vmm_only=False):
+        if not vmm_only:
+            for y in ys.values():
+                y.zero_()
         for t in range(T):
             c = copies[t % R]
             if not vmm_only:
@@ -419,7 +422,7 @@ def run_lut(args, torch, g, wl_name, wl):
                                     thresholds=thresholds[xin], out=lm[xin][t:t + 1])
             for name, _, _, xin, _ in layers:
                 g.grinqh_vmm_lut(descs[name], c[name][0], c[name][1], xs[xin][t:t + 1],
-                                 lm[xin][t:t + 1], y=ys[name][t:t + 1])
+                                 lm[xin][t:t + 1], y=ys[name][t:t + 1], accumulate=True)
 
     s = torch.cuda.Stream()
     s.wait_stream(torch.cuda.current_stream())

@@ -129,5 +129,30 @@ __device__ __forceinline__ float lane_group_sum(float v) {
   }
 }
 
+// Bit o of a 16-bit word moved to bit 2o.
+__device__ __forceinline__ uint32_t spread_bits(uint32_t v) {
+  v = (v | (v << 8)) & 0x00FF00FFu;
+  v = (v | (v << 4)) & 0x0F0F0F0Fu;
+  v = (v | (v << 2)) & 0x33333333u;
+  return (v | (v << 1)) & 0x55555555u;
+}
+
+// The codes of 16 outputs from the four 2-bit plane words (output o's field
+// at bit 2o, plane 1 most significant): byte i of q[d] is the code of output
+// 4i + d.
+__device__ __forceinline__ void assemble_codes(uint32_t w1, uint32_t w2, uint32_t w3, uint32_t w4,
+                                               uint32_t (&q)[4]) {
+  // 4-bit fields of the even (E) and odd (O) outputs: output 2m or 2m+1 at
+  // bits 4m..4m+3, the first plane of the pair on top
+  const uint32_t E12 = ((w1 << 2) & 0xCCCCCCCCu) | (w2 & 0x33333333u);
+  const uint32_t O12 = (w1 & 0xCCCCCCCCu) | ((w2 >> 2) & 0x33333333u);
+  const uint32_t E34 = ((w3 << 2) & 0xCCCCCCCCu) | (w4 & 0x33333333u);
+  const uint32_t O34 = (w3 & 0xCCCCCCCCu) | ((w4 >> 2) & 0x33333333u);
+  q[0] = ((E12 & 0x0F0F0F0Fu) << 4) | (E34 & 0x0F0F0F0Fu);
+  q[1] = ((O12 & 0x0F0F0F0Fu) << 4) | (O34 & 0x0F0F0F0Fu);
+  q[2] = (E12 & 0xF0F0F0F0u) | ((E34 >> 4) & 0x0F0F0F0Fu);
+  q[3] = (O12 & 0xF0F0F0F0u) | ((O34 >> 4) & 0x0F0F0F0Fu);
+}
+
 }  // namespace vmmdev
 }  // namespace grinqh

@@ -16,6 +16,7 @@
 #include <cstdlib>
 
 #include "grinqh_internal.h"
+#include "vmm_common.h"
 
 namespace grinqh {
 
@@ -36,7 +37,7 @@ __global__ __launch_bounds__(kLutThreads) void k_vmm_lut(const uint8_t* __restri
                                                         const uint16_t* __restrict__ x,
                                                         const uint8_t* __restrict__ lm,
                                                         float* __restrict__ y, Layer L, LutDesc D,
-                                                        int groups_per_split) {
+                                                        int groups_per_split, int splits) {
   constexpr uint32_t MASK = (1u << U) - 1u;
   extern __shared__ __align__(16) uint16_t s_lut[];          // [levels][kSub][2^b]
   __shared__ float s_red[kLutThreads / 64][kSub];
@@ -44,9 +45,16 @@ __global__ __launch_bounds__(kLutThreads) void k_vmm_lut(const uint8_t* __restri
   __shared__ uint8_t s_lv[kMaxRun];                           // levels of the run's channels
   __shared__ uint16_t s_x[kMaxRun];                           // x of the run's channels
 
+  // Work order: the K splits of a sub-tile, then the sub-tiles of a tile,
+  // are consecutive work items, and consecutive items run on one XCD
+  // (workgroup id mod 8 picks the XCD): its L2 then serves the sub-tiles'
+  // shared 128-byte plane lines and the splits' shared tables.
   const int subs = L.T / kSub;
-  const int tile_sub = blockIdx.x % (L.tiles * subs);
-  const int split = blockIdx.x / (L.tiles * subs);
+  const int nwg = gridDim.x;
+  const int item = (nwg % 8 == 0) ? (int)(blockIdx.x % 8) * (nwg / 8) + (int)(blockIdx.x / 8)
+                                  : (int)blockIdx.x;
+  const int tile_sub = item / splits;
+  const int split = item % splits;
   const int t = tile_sub / subs, sub = tile_sub % subs;
   const int tok = blockIdx.y;
   const int n0 = t * L.T + sub * kSub;       // first output of the sub-tile
@@ -109,21 +117,28 @@ __global__ __launch_bounds__(kLutThreads) void k_vmm_lut(const uint8_t* __restri
       const float xv = h2f(s_x[i]);
       const int d = level_planes(L.planes_packed, lvl);
       const int b = d * U;
-      uint32_t q[16];
+      // the 16 outputs' codes left-aligned in 8 bits (planes past d are
+      // zero): byte i of qw[r] is output 4 i + r; q_b is its top b bits
+      uint32_t w[4];
+      if constexpr (U == 2) {
 #pragma unroll
-      for (int e = 0; e < 16; ++e) q[e] = 0u;
+        for (int j = 0; j < 4; ++j) w[j] = wa[j];
+      } else {
 #pragma unroll
-      for (int j = 0; j < kWords; ++j) {
-        if (j < d) {
-#pragma unroll
-          for (int e = 0; e < 16; ++e) q[e] = (q[e] << U) | ((wa[j] >> (e * U)) & MASK);
-        }
+        for (int j = 0; j < 4; ++j)
+          w[j] = (vmmdev::spread_bits(wa[2 * j]) << 1) | vmmdev::spread_bits(wa[2 * j + 1]);
       }
+      uint32_t qw[4];
+      vmmdev::assemble_codes(w[0], w[1], w[2], w[3], qw);
+      const int sh = 8 - b;
       // the lane's outputs' rows of level lvl's table: output 16 c + e at
-      // (16 c + e) * 2^b, q_b = q[e] below it
+      // (16 c + e) * 2^b
       const uint16_t* tb = s_lut + kSub * s_cum[lvl] + ((16 * c) << b);
 #pragma unroll
-      for (int e = 0; e < 16; ++e) acc[e] = fmaf(xv, h2f(tb[(e << b) + q[e]]), acc[e]);
+      for (int e = 0; e < 16; ++e) {
+        const uint32_t q8 = (qw[e & 3] >> (8 * (e >> 2))) & 0xFFu;
+        acc[e] = fmaf(xv, h2f(tb[(e << b) + (q8 >> sh)]), acc[e]);
+      }
     }
 #pragma unroll
     for (int j = 0; j < kWords; ++j) wa[j] = wb[j];
@@ -175,11 +190,14 @@ int launch_vmm_lut(const Layer& L, const void* codes, const void* luts, const vo
     const long n = (long)B * L.N;
     hipLaunchKernelGGL(k_zero_lut, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, y, n);
   }
-  // about two workgroups per CU over (sub-tiles x K splits x tokens)
+  // about four workgroups per CU over (sub-tiles x K splits x tokens), each
+  // taking 4..16 groups: fewer groups re-copy the tables too often, fewer
+  // workgroups hide too little latency (measured on the Llama3-8B shapes)
   const long subtiles = (long)L.tiles * (L.T / kSub);
-  long splits = (512 + subtiles * B - 1) / (subtiles * B);
-  splits = splits < 1 ? 1 : (splits > L.groups ? L.groups : splits);
-  int gps = (int)((L.groups + splits - 1) / splits);
+  long splits;
+  int gps = (int)(((long)L.groups * subtiles * B + 1023) / 1024);
+  gps = gps < 4 ? 4 : (gps > 16 ? 16 : gps);
+  gps = gps > L.groups ? L.groups : gps;
   if (const char* e = getenv("GRINQH_LUT_GPS")) {
     const int v = atoi(e);
     if (v >= 1 && v <= L.groups) gps = v;
@@ -189,10 +207,10 @@ int launch_vmm_lut(const Layer& L, const void* codes, const void* luts, const vo
   const dim3 grid((unsigned)(subtiles * splits), (unsigned)B);
   if (L.u == 2)
     hipLaunchKernelGGL(k_vmm_lut<2>, grid, dim3(kLutThreads), lds, s, (const uint8_t*)codes,
-                       (const uint16_t*)luts, (const uint16_t*)x, level_map, y, L, D, gps);
+                       (const uint16_t*)luts, (const uint16_t*)x, level_map, y, L, D, gps, (int)splits);
   else
     hipLaunchKernelGGL(k_vmm_lut<1>, grid, dim3(kLutThreads), lds, s, (const uint8_t*)codes,
-                       (const uint16_t*)luts, (const uint16_t*)x, level_map, y, L, D, gps);
+                       (const uint16_t*)luts, (const uint16_t*)x, level_map, y, L, D, gps, (int)splits);
   return check_launch("vmm_lut");
 }
 
