@@ -38,8 +38,8 @@ using namespace vmmdev;
 
 constexpr int kMaxGW = 4;                    // groups per workgroup (B = 1)
 constexpr int max_gw(int nb) { return nb == 1 ? kMaxGW : 2; }   // LDS of the pair lists
-constexpr int kMaxItems = kGroup * 4;        // 128 rows x 4 planes
-constexpr int kMaxPairs = kMaxItems / 2;
+// plane rows of a group: 128 rows x 8/U planes (4 two-bit or 8 one-bit planes)
+constexpr int max_pairs(int u) { return kGroup * (8 / u) / 2; }
 
 // Per-pair descriptor: byte offsets of the two plane chunks from the tile
 // base, the fp16x2 exponent bits for field position 4, and one fp16x2
@@ -49,7 +49,7 @@ struct Desc {
   static constexpr int DW = NB == 1 ? 4 : 8;
 };
 
-template <int V, int LPR, int NB, int PB, int kThreads>
+template <int U, int V, int LPR, int NB, int PB, int kThreads>
 __global__ __launch_bounds__(kThreads) void k_vmm_dot2(
     const uint8_t* __restrict__ codes, const uint16_t* __restrict__ scales,
     const uint16_t* __restrict__ x, const uint8_t* __restrict__ lm, float* __restrict__ y,
@@ -60,7 +60,7 @@ __global__ __launch_bounds__(kThreads) void k_vmm_dot2(
   constexpr int kWaves = kThreads / 64;
   constexpr int DW = Desc<NB>::DW;
 
-  __shared__ __align__(16) uint32_t s_pairs[max_gw(NB)][kMaxPairs][DW];
+  __shared__ __align__(16) uint32_t s_pairs[max_gw(NB)][max_pairs(U)][DW];
   __shared__ __align__(16) uint32_t s_empty[kThreads / LPR * PB][DW];   // one all-empty batch
   __shared__ int s_npairs[max_gw(NB)];
   __shared__ float s_beta[max_gw(NB)][NB];
@@ -132,19 +132,19 @@ __global__ __launch_bounds__(kThreads) void k_vmm_dot2(
       db[b] = level_planes(L.planes_packed, lb);
       D0 = max(D0, da[b]);
       D1 = max(D1, db[b]);
-      beta[b] = (la ? fa * phi_minus_offset(2 * da[b], L.bmax) : 0.0f) +
-                (lb ? fb * phi_minus_offset(2 * db[b], L.bmax) : 0.0f);
+      beta[b] = (la ? fa * phi_minus_offset(U * da[b], L.bmax) : 0.0f) +
+                (lb ? fb * phi_minus_offset(U * db[b], L.bmax) : 0.0f);
     }
     const int cnt = D0 + D1;
     const int np = (cnt + 1) >> 1;
     int pos = 0, total = 0;
 #pragma unroll
-    for (int q = 1; q <= 4; ++q) {
+    for (int q = 1; q <= 8 / U; ++q) {
       pos += lanes_below(np >= q);
       total += lanes_total(np >= q);
     }
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
+    for (int q = 0; q < 8 / U; ++q) {
       if (2 * q >= cnt) break;
       // items 2q and 2q+1 of the lane: item i is (row r0, plane i+1) below D0,
       // else (row r0+1, plane i-D0+1)
@@ -154,9 +154,10 @@ __global__ __launch_bounds__(kThreads) void k_vmm_dot2(
       const int rb = ib < D0 ? 0 : 1, jb = has_b ? (ib < D0 ? ib + 1 : ib - D0 + 1) : ja;
       const int rbb = has_b ? rb : ra;
       uint32_t* d = s_pairs[gg][pos + q];
-      d[0] = (uint32_t)((k0 + ra) * L.RB + (ja - 1) * (T / 4));
-      d[1] = (uint32_t)((k0 + rbb) * L.RB + (jb - 1) * (T / 4));
-      d[2] = ((uint32_t)(29 - 2 * ja) << 10) | ((uint32_t)(29 - 2 * jb) << 26);
+      // plane j of width U is worth 2^(8 - U j) code units: exponent base 29 - U j
+      d[0] = (uint32_t)((k0 + ra) * L.RB + (ja - 1) * (T * U / 8));
+      d[1] = (uint32_t)((k0 + rbb) * L.RB + (jb - 1) * (T * U / 8));
+      d[2] = ((uint32_t)(29 - U * ja) << 10) | ((uint32_t)(29 - U * jb) << 26);
 #pragma unroll
       for (int b = 0; b < NB; ++b) {
         const uint32_t xa = ra ? (xxs[b] >> 16) : (xxs[b] & 0xFFFFu);
@@ -202,7 +203,7 @@ __global__ __launch_bounds__(kThreads) void k_vmm_dot2(
   // of the next batch are in flight while the current one is consumed, across
   // group boundaries too.  A group with no pairs still gets one (empty) batch
   // so its epilogue runs and the scale prefetch advances.
-  const uint8_t* tile = codes + (size_t)t * L.K * L.RB + li * 4 * V;
+  const uint8_t* tile = codes + (size_t)t * L.K * L.RB + li * 2 * U * V;   // 16 V outputs per lane
   float yp[NB][NACC], acc[NB][NACC], off[NB];
 #pragma unroll
   for (int b = 0; b < NB; ++b) {
@@ -257,8 +258,19 @@ __global__ __launch_bounds__(kThreads) void k_vmm_dot2(
 #pragma unroll
         for (int b = 0; b < NB; ++b) B.xp[q][b] = cw[b];
       }
-      const Words<V> u1 = load_words<V>(tile + a.x);
-      const Words<V> u2 = load_words<V>(tile + a.y);
+      Words<V> u1, u2;
+      if constexpr (U == 2) {
+        u1 = load_words<V>(tile + a.x);
+        u2 = load_words<V>(tile + a.y);
+      } else {
+        // sixteen 1-bit fields moved to bit 2o: the 2-bit field machinery then
+        // reads each as 0 or 1 at the plane's own weight
+#pragma unroll
+        for (int v = 0; v < V; ++v) {
+          u1.w[v] = spread_bits(__builtin_nontemporal_load((const uint16_t*)(tile + a.x) + v));
+          u2.w[v] = spread_bits(__builtin_nontemporal_load((const uint16_t*)(tile + a.y) + v));
+        }
+      }
 #pragma unroll
       for (int v = 0; v < V; ++v) {
         B.w1[q][v] = u1.w[v];
@@ -352,21 +364,22 @@ __global__ __launch_bounds__(kThreads) void k_vmm_dot2(
   }
 }
 
-template <int V, int LPR, int NB, int NT>
+template <int U, int V, int LPR, int NB, int NT>
 void launch_one(dim3 grid, hipStream_t s, const void* codes, const void* scales, const void* x,
                 const uint8_t* lm, float* y, const Layer& L, int gw, int fused,
                 const Thresholds& th, uint8_t* lm_out) {
   constexpr int PB = (V == 1 && NB <= 2) ? 4 : 2;   // pairs per batch; four batches in flight
-  hipLaunchKernelGGL((k_vmm_dot2<V, LPR, NB, PB, NT>), grid, dim3(NT), 0, s, (const uint8_t*)codes,
+  hipLaunchKernelGGL((k_vmm_dot2<U, V, LPR, NB, PB, NT>), grid, dim3(NT), 0, s, (const uint8_t*)codes,
                      (const uint16_t*)scales, (const uint16_t*)x, lm, y, L, gw, fused, th, lm_out);
 }
 
 }  // namespace
 
-// Tiles of 256, 512 or 1024 outputs: one dword (16 outputs) per lane and
-// plane row, so 16, 32 or 64 lanes cover a plane row.
+// Tiles of 256, 512 or 1024 outputs (512 or 1024 for 1-bit planes): 16
+// outputs per lane and plane row, so 16, 32 or 64 lanes cover a plane row.
 bool vmm_dot2_supported(const Layer& L) {
-  return L.u == 2 && (L.T == 256 || L.T == 512 || L.T == 1024);
+  if (L.u == 2) return L.T == 256 || L.T == 512 || L.T == 1024;
+  return L.T == 512 || L.T == 1024;
 }
 
 int vmm_dot2_groups_per_wg(const Layer& L) {
@@ -391,20 +404,22 @@ int launch_vmm_dot2(const Layer& L, const void* codes, const void* scales, const
   const int fused = th != nullptr;
   const char* env_nt = getenv("GRINQH_VMM_THREADS");
   const int nt = (env_nt && atoi(env_nt) == 512 && B == 1) ? 512 : 256;
-  if (nt == 512) {
-    if (L.T == 256) launch_one<1, 16, 1, 512>(grid, s, codes, scales, x, level_map, y, L, gw, fused, tt, level_map_out);
-    else if (L.T == 512) launch_one<1, 32, 1, 512>(grid, s, codes, scales, x, level_map, y, L, gw, fused, tt, level_map_out);
-    else launch_one<1, 64, 1, 512>(grid, s, codes, scales, x, level_map, y, L, gw, fused, tt, level_map_out);
+  if (nt == 512 && L.u == 2) {
+    if (L.T == 256) launch_one<2, 1, 16, 1, 512>(grid, s, codes, scales, x, level_map, y, L, gw, fused, tt, level_map_out);
+    else if (L.T == 512) launch_one<2, 1, 32, 1, 512>(grid, s, codes, scales, x, level_map, y, L, gw, fused, tt, level_map_out);
+    else launch_one<2, 1, 64, 1, 512>(grid, s, codes, scales, x, level_map, y, L, gw, fused, tt, level_map_out);
     return check_launch("vmm (dot2)");
   }
-#define GRINQH_DOT2_CASE(TT, LL, NN)                                                              \
-  if (L.T == TT && B == NN) {                                                                    \
-    launch_one<1, LL, NN, 256>(grid, s, codes, scales, x, level_map, y, L, gw, fused, tt, level_map_out); \
+#define GRINQH_DOT2_CASE(UU, TT, LL, NN)                                                          \
+  if (L.u == UU && L.T == TT && B == NN) {                                                       \
+    launch_one<UU, 1, LL, NN, 256>(grid, s, codes, scales, x, level_map, y, L, gw, fused, tt, level_map_out); \
     return check_launch("vmm (dot2)");                                                           \
   }
-  GRINQH_DOT2_CASE(256, 16, 1) GRINQH_DOT2_CASE(256, 16, 2) GRINQH_DOT2_CASE(256, 16, 3) GRINQH_DOT2_CASE(256, 16, 4)
-  GRINQH_DOT2_CASE(512, 32, 1) GRINQH_DOT2_CASE(512, 32, 2) GRINQH_DOT2_CASE(512, 32, 3) GRINQH_DOT2_CASE(512, 32, 4)
-  GRINQH_DOT2_CASE(1024, 64, 1) GRINQH_DOT2_CASE(1024, 64, 2) GRINQH_DOT2_CASE(1024, 64, 3) GRINQH_DOT2_CASE(1024, 64, 4)
+  GRINQH_DOT2_CASE(2, 256, 16, 1) GRINQH_DOT2_CASE(2, 256, 16, 2) GRINQH_DOT2_CASE(2, 256, 16, 3) GRINQH_DOT2_CASE(2, 256, 16, 4)
+  GRINQH_DOT2_CASE(2, 512, 32, 1) GRINQH_DOT2_CASE(2, 512, 32, 2) GRINQH_DOT2_CASE(2, 512, 32, 3) GRINQH_DOT2_CASE(2, 512, 32, 4)
+  GRINQH_DOT2_CASE(2, 1024, 64, 1) GRINQH_DOT2_CASE(2, 1024, 64, 2) GRINQH_DOT2_CASE(2, 1024, 64, 3) GRINQH_DOT2_CASE(2, 1024, 64, 4)
+  GRINQH_DOT2_CASE(1, 512, 32, 1) GRINQH_DOT2_CASE(1, 512, 32, 2) GRINQH_DOT2_CASE(1, 512, 32, 3) GRINQH_DOT2_CASE(1, 512, 32, 4)
+  GRINQH_DOT2_CASE(1, 1024, 64, 1) GRINQH_DOT2_CASE(1, 1024, 64, 2) GRINQH_DOT2_CASE(1, 1024, 64, 3) GRINQH_DOT2_CASE(1, 1024, 64, 4)
 #undef GRINQH_DOT2_CASE
   return fail(GRINQH_EUNSUPPORTED, "dot2 VMM: no kernel for tile %d, B=%d", L.T, B);
 }

@@ -532,8 +532,6 @@ def test_pack_bmax_bit_exact(g, torch, levels, codes_src):
 def test_vmm_bmax_random_level_maps(g, torch, levels, kernel, monkeypatch):
     if kernel != "auto":
         monkeypatch.setenv("GRINQH_VMM_KERNEL", kernel)
-    if kernel == "dot2" and orc.plane_bits_for(levels) == 1:
-        pytest.skip("the per-plane kernels read 2-bit planes")
     K, N = 1152, 1024
     L = Layer(g, torch, K, N, levels, cfg=81, codes_src=True)
     rng = np.random.default_rng(81)
@@ -676,3 +674,24 @@ def test_vmm_lut_accumulate(g, torch):
     yd = _dev(torch, base)
     L.run(g, torch, x, lm, y=yd, accumulate=True)
     assert normwise(_host(yd), L.ref(x, lm) + base) <= TOL
+
+
+@pytest.mark.parametrize("levels", [(0, 2, 3, 4, 8), (0, 1, 2, 3, 4), (0, 3, 6)])
+@pytest.mark.parametrize("tile_n", [512, 1024])
+def test_vmm_one_bit_planes_dot2(g, torch, levels, tile_n, monkeypatch):
+    # 1-bit planes through the per-plane kernel: each plane a work item at
+    # its own weight, per-token depths exact for B > 1
+    monkeypatch.setenv("GRINQH_VMM_KERNEL", "dot2")
+    K, N = 1152, 2048
+    L = Layer(g, torch, K, N, levels, cfg=84, layer=tile_n, tile_n=tile_n)
+    assert L.desc.plane_bits == 1
+    rng = np.random.default_rng(tile_n)
+    for B in (1, 2, 3, 4):
+        x = inputs.activations_t3(K, B, 84, B)
+        lm = rng.integers(0, len(levels), size=(B, K)).astype(np.uint8)
+        y, ref = _vmm_case(g, torch, L, x, lm)
+        assert normwise(y, ref) <= TOL, (B, normwise(y, ref))
+    th = np.sort(np.abs(x[0].astype(np.float32)))[[300, 600, 900, 1100][:len(levels) - 1]]
+    y = g.grinqh_vmm_threshold(L.desc, L.pc, L.ps, _dev(torch, x), th)
+    torch.cuda.synchronize()
+    assert normwise(_host(y), orc.vmm_batch(L.codes, L.scales, x, orc.assign_threshold(x, th), levels)) <= TOL
