@@ -20,6 +20,18 @@ __device__ __forceinline__ int lanes_below(bool pred) {
 }
 __device__ __forceinline__ int lanes_total(bool pred) { return (int)__popcll(__ballot(pred)); }
 
+// The same over this lane's half wave (lanes 0..31 or 32..63); the low mask
+// is zeroed for the upper half, so both counts run unbranched.
+__device__ __forceinline__ int half_below(bool pred) {
+  const uint64_t m = __ballot(pred);
+  const uint32_t lo = (threadIdx.x & 32) ? 0u : (uint32_t)m;
+  return (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo(lo, 0u));
+}
+__device__ __forceinline__ int half_total(bool pred) {
+  const uint64_t m = __ballot(pred);
+  return (threadIdx.x & 32) ? __popc((uint32_t)(m >> 32)) : __popc((uint32_t)m);
+}
+
 // Sixteen outputs of one pair: w1/w2 are the two plane rows' dwords.
 template <int NB, int NACC>
 __device__ __forceinline__ void consume_pair(uint32_t w1, uint32_t w2, uint32_t m4,
@@ -112,6 +124,18 @@ __device__ __forceinline__ float wave_sum_dpp(float v) {
   v += row_ror<2>(v);
   v += row_ror<1>(v);
   return row_sum4(v);
+}
+
+// Sum over this lane's half wave, in every lane of it: row sums by rotation,
+// then rows r and r^1.
+__device__ __forceinline__ float half_sum_dpp(float v) {
+  v += row_ror<8>(v);
+  v += row_ror<4>(v);
+  v += row_ror<2>(v);
+  v += row_ror<1>(v);
+  uint32_t a = __builtin_bit_cast(uint32_t, v), b = a;
+  asm volatile("s_nop 1\n\tv_permlane16_swap_b32 %0, %1" : "+v"(a), "+v"(b));
+  return __builtin_bit_cast(float, a) + __builtin_bit_cast(float, b);
 }
 
 // Sum over the lane groups of a wave that hold the same outputs: LPR lanes

@@ -24,7 +24,14 @@
 //   y_n += s_{g,n} (acc_n - f_d(n) off_d - f_s(n) off_s + beta_g),
 // with f_d = 2^(-p) for doubles, f_s = 2^(4-p) for singles (p = the output's
 // field position) and beta_g = sum_{k: level > 0} x_k (phi_b - 128).
+//
+// The prologue is spread over the four waves (each half wave grades 32 rows
+// of a group; per-wave item counts are exchanged through LDS).
+// With the plane-1 read-ahead, plane 1 of the first group's 128 rows is requested
+// before x arrives and consumed as singles, and that group's lists start at
+// plane 2: doubles (2,3) and an even last plane as a single.
 #include <cstdlib>
+#include <type_traits>
 
 #include "grinqh_internal.h"
 #include "vmm_common.h"
@@ -35,9 +42,6 @@ namespace {
 
 using namespace vmmdev;
 
-#ifndef GRINQH_PP_PREFETCH
-#define GRINQH_PP_PREFETCH false
-#endif
 #ifndef GRINQH_PP_DEPTH
 #define GRINQH_PP_DEPTH 4
 #endif
@@ -80,7 +84,7 @@ __device__ __forceinline__ float double_offset_factor(int e) {
   return ((e >> 1) & 1) ? 0.0625f : 1.0f;
 }
 
-template <int LPR, int PB, int D, int kThreads, bool PREFETCH>
+template <int LPR, int PB, int D, int kThreads, bool SPEC>
 __global__ __launch_bounds__(kThreads) void k_vmm_pp(
     const uint8_t* __restrict__ codes, const uint16_t* __restrict__ scales,
     const uint16_t* __restrict__ x, const uint8_t* __restrict__ lm, float* __restrict__ y,
@@ -97,6 +101,9 @@ __global__ __launch_bounds__(kThreads) void k_vmm_pp(
   __shared__ float s_beta[kPPMaxGW];
   __shared__ __align__(16) uint16_t s_scale[kPPMaxGW][T];
   __shared__ __align__(16) float s_red[kWaves][T];
+  __shared__ uint32_t s_spx[kGroup / 2];   // read-ahead rows' x pairs, 0 for level 0
+  __shared__ int s_cnt[kPPMaxGW][kWaves][2];   // items (doubles, singles) per group and wave
+  __shared__ float s_bpart[kPPMaxGW][kWaves];  // beta_g partial sums per wave
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int t = blockIdx.x % L.tiles;
@@ -105,132 +112,105 @@ __global__ __launch_bounds__(kThreads) void k_vmm_pp(
   const int n_top = L.n_levels - 1;
   const int lg = tid / LPR, li = tid % LPR;
 
-  // Before anything else, touch plane 1 of the first group's 128 rows, one
-  // dword per 128-byte line, so that the main loop finds these lines in L2
-  // instead of waiting a memory latency for them after the prologue.  Every
-  // channel above level 0 reads plane 1; the lines of level-0 rows are the
-  // only bytes fetched without need.  The load is written as asm so that
-  // nothing waits for it: its destination register stays live (and unread)
-  // until the single wait at the end of the kernel.  The compiler's own
-  // waits count this older load too, which only makes them stricter.
-  uint32_t pf = 0;
-  if constexpr (PREFETCH) {
-    constexpr int kLinesPerRow = PLANE >= 128 ? PLANE / 128 : 1;
-    constexpr int kRowsPerLine = PLANE >= 128 ? 1 : 128 / PLANE;
-    constexpr int kLines = kGroup * kLinesPerRow / kRowsPerLine;   // <= kThreads
-    const int i = tid % kLines;   // threads past kLines repeat a line
-    const int r = (i / kLinesPerRow) * kRowsPerLine, c = i % kLinesPerRow;
-    const uint8_t* a = codes + (size_t)t * L.K * L.RB + (size_t)(g0 * kGroup + r) * L.RB + c * 128;
-    asm volatile("global_load_dword %0, %1, off" : "=v"(pf) : "v"(a) : "memory");
+  // ---- prologue.  The four waves grade the rows together: in pass i, lane
+  // l of wave w takes row 32w + (l & 31) of group 2i + (l >> 5), so each half
+  // wave covers 32 rows of one group.  A group's items go into its unit
+  // list, doubles first (item i -> unit i/2, channel slot i%2), then singles
+  // (item i -> unit (doubles padded) + i/4, pair (i/2)%2, slot i%2); a half
+  // wave's items follow those of the lower waves' halves of the same group,
+  // whose counts are exchanged through LDS.  (Whole waves of 64 rows, two
+  // waves per group, measured slower: the prologue is a chain of dependent
+  // instructions, so halving the rows per wave halves its latency.)
+  static_assert(kWaves == 4 && kGroup == 128, "32 rows per half wave");
+  constexpr int kPasses = (kPPMaxGW + 1) / 2;
+  constexpr int SH = T / 256;                // scale halves per lane and group
+  const int half = lane >> 5, hl = lane & 31;
+  const int row = 32 * wave + hl;            // row of the group
+  // x, the level map and the scales are requested together, so the
+  // prologue waits for one memory latency, not two
+  uint32_t xv[kPasses], lv[kPasses];
+  using ScaleWord = typename std::conditional<SH == 4, uint2, typename std::conditional<SH == 2, uint32_t, uint16_t>::type>::type;
+  ScaleWord scw[kPPMaxGW];
+  // (unconditional loads, so that the compiler counts them exactly and
+  // waits for x alone before grading; groups past the workgroup's last one
+  // read that one again, from cache)
+  const uint8_t* lmsrc = fused ? (const uint8_t*)x : lm;   // in fused mode the read is ignored
+#pragma unroll
+  for (int i = 0; i < kPasses; ++i) {
+    const int k = (g0 + min(2 * i + half, ng - 1)) * kGroup + row;
+    xv[i] = x[k];
+    lv[i] = lmsrc[k];
   }
+#pragma unroll
+  for (int gg = 0; gg < kPPMaxGW; ++gg)
+    scw[gg] = *(const ScaleWord*)(scales + (size_t)(g0 + min(gg, ng - 1)) * L.N + (size_t)t * T +
+                                  (wave * 64 + lane) * SH);
 
-  // ---- prologue: one wave per group, lane l grades rows 2l and 2l+1 and
-  // writes its items straight into the group's unit list at ballot prefix
-  // positions.  Doubles: item i -> unit i/2, channel slot i%2.  Singles: item
-  // i -> unit (doubles padded) + i/4, pair (i/2)%2, channel slot i%2.
-  for (int gg = wave; gg < ng; gg += kWaves) {
-    const int g = g0 + gg;
-    const int r0 = 2 * lane;
-    const int k0 = g * kGroup + r0;
-    // x, the level map and the scales are requested together, so the
-    // prologue waits for one memory latency, not two
-    const uint8_t* lmsrc = fused ? (const uint8_t*)x : lm;   // in fused mode the read is ignored
-    const uint32_t xx = *(const uint32_t*)(x + k0);
-    const uint16_t ll = *(const uint16_t*)(lmsrc + k0);
-    {   // this group's scales for the tile: T fp16 = 64 lanes x T/64 halves
-      constexpr int H = T / 64;
-      const uint16_t* sp = scales + (size_t)g * L.N + (size_t)t * T + lane * H;
-      if constexpr (H == 4) {
-        *(uint2*)&s_scale[gg][lane * H] = *(const uint2*)sp;
-      } else {
+  // Read-ahead: every channel above level 0 reads plane 1, so plane 1 of the
+  // first group's 128 rows is requested now, behind x, and arrives while the
+  // prologue waits for x and builds the lists; only level-0 rows' bytes are
+  // fetched without need.  Unit u holds rows 4u..4u+3 (two pairs); lane group
+  // lg takes units lg, lg + kLaneGroups, ...  The lists then hold the planes
+  // 2..d of those rows.
+  constexpr int kSpecUnits = kGroup / 4;
+  constexpr int kSpecPerLG = SPEC ? kSpecUnits / kLaneGroups : 0;
+  static_assert(!SPEC || kSpecUnits % kLaneGroups == 0, "read-ahead units per lane group");
+  uint32_t spw[kSpecPerLG > 0 ? 4 * kSpecPerLG : 1];
+  const uint8_t* tile = codes + (size_t)t * L.K * L.RB;
+  const uint32_t li4 = (uint32_t)li * 4u;
+  if constexpr (SPEC) {
 #pragma unroll
-        for (int c = 0; c < H / 8; ++c) *(uint4*)&s_scale[gg][lane * H + 8 * c] = *(const uint4*)(sp + 8 * c);
-      }
-    }
-    asm volatile("" ::"v"(ll));   // the level-map load is issued before the wait above
-    const float fa = h2f((uint16_t)(xx & 0xFFFFu)), fb = h2f((uint16_t)(xx >> 16));
-    int la, lb;
-    if (fused) {
-      la = 0;
-      lb = 0;
-      const float aa = fabsf(fa), ab = fabsf(fb);
+    for (int q = 0; q < kSpecPerLG; ++q) {
+      const int r = 4 * (lg + kLaneGroups * q);
 #pragma unroll
-      for (int j = 0; j < kMaxLevels - 1; ++j) {   // unrolled: the thresholds are one scalar load
-        la += (j < th.n && aa >= th.theta[j]) ? 1 : 0;
-        lb += (j < th.n && ab >= th.theta[j]) ? 1 : 0;
-      }
-      if (lm_out && t == 0) *(uint16_t*)(lm_out + k0) = (uint16_t)(la | (lb << 8));
-    } else {
-      la = min((int)(ll & 0xFFu), n_top);
-      lb = min((int)(ll >> 8), n_top);
+      for (int i = 0; i < 4; ++i)
+        spw[4 * q + i] = __builtin_nontemporal_load(
+            (const uint32_t*)(tile + ((uint32_t)(g0 * kGroup + r + i) * (uint32_t)L.RB + li4)));
     }
-    const int da = level_planes(L.planes_packed, la), db = level_planes(L.planes_packed, lb);
-    const float beta = (la ? fa * phi_minus_offset(2 * da, L.bmax) : 0.0f) +
-                       (lb ? fb * phi_minus_offset(2 * db, L.bmax) : 0.0f);
-    const int nda = da >> 1, ndb = db >> 1;      // doubles of each row
-    const int nsa = da & 1, nsb = db & 1;        // singles of each row
-    const int nd = nda + ndb, ns = nsa + nsb;
-    int dpos = 0, dtot = 0, spos = 0, stot = 0;
+  }
+  __builtin_amdgcn_sched_barrier(0);
+
+  // grade, count items, local positions
+  int dep[kPasses], ndb[kPasses], nsg[kPasses], dpos[kPasses], spos[kPasses];
 #pragma unroll
-    for (int q = 1; q <= 4; ++q) {
-      dpos += lanes_below(nd >= q);
-      dtot += lanes_total(nd >= q);
-    }
+  for (int i = 0; i < kPasses; ++i) {
+    if (i > 0 && 2 * i >= ng) break;         // uniform: the groups of this pass are absent
+    const int gg = 2 * i + half;
+    const bool valid = gg < ng;
+    const float fx = h2f((uint16_t)xv[i]);
+    // graded from x (th.n is 0 without thresholds) or read from the level
+    // map, chosen without a branch so that the level-map load stays early
+    int graded = 0;
+    const float ax = fabsf(fx);
 #pragma unroll
-    for (int q = 1; q <= 2; ++q) {
-      spos += lanes_below(ns >= q);
-      stot += lanes_total(ns >= q);
+    for (int j = 0; j < kMaxLevels - 1; ++j) {
+      if (j >= th.n) break;                  // uniform
+      graded += ax >= th.theta[j] ? 1 : 0;
     }
-    const int n_du = (dtot + 1) >> 1, n_su = (stot + 3) >> 2;
-    const int pad_du = (n_du + kSlots - 1) / kSlots * kSlots;
-    int pad_su = (n_su + kSlots - 1) / kSlots * kSlots;
-    if (pad_du + pad_su == 0) pad_su = kSlots;   // an empty group still gets one batch
-    uint32_t* U = &s_units[gg][0][0];
-    const uint32_t xa = xx & 0xFFFFu, xb = xx >> 16;
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      if (q >= nd) break;
-      const bool ra = q < nda;
-      const int j = 2 * (ra ? q : q - nda) + 1;               // first plane of the pair
-      const uint32_t off = (uint32_t)((k0 + (ra ? 0 : 1)) * L.RB + (j - 1) * PLANE);
-      const int i = dpos + q, u = i >> 1, h = i & 1;
-      U[u * 8 + h] = off;
-      U[u * 8 + 4 + h] = off + PLANE;
-      reinterpret_cast<uint16_t*>(&U[u * 8 + 2])[h] = (uint16_t)((31 - 2 * j) << 10);
-      reinterpret_cast<uint16_t*>(&U[u * 8 + 3])[h] = (uint16_t)(ra ? xa : xb);
+    const int lvl = fused ? graded : min((int)(lv[i] & 0xFFu), n_top);
+    if (fused && lm_out && t == 0 && valid) lm_out[(g0 + gg) * kGroup + row] = (uint8_t)lvl;
+    const int d = valid ? level_planes(L.planes_packed, lvl) : 0;
+    // planes to list: all d of them, or 2..d when plane 1 was read ahead;
+    // doubles of consecutive planes from the first listed one, and a single
+    // for a last plane left over
+    const bool sg = SPEC && gg == 0;
+    const int jl = sg ? max(d - 1, 0) : d;
+    dep[i] = d;
+    ndb[i] = jl >> 1;
+    nsg[i] = jl & 1;
+    const float beta = d ? fx * phi_minus_offset(2 * d, L.bmax) : 0.0f;
+    const int d1 = half_below(ndb[i] >= 1), d2 = half_below(ndb[i] >= 2);
+    const int dt = half_total(ndb[i] >= 1) + half_total(ndb[i] >= 2);
+    dpos[i] = d1 + d2;
+    spos[i] = half_below(nsg[i] >= 1);
+    const int st = half_total(nsg[i] >= 1);
+    const float bs = half_sum_dpp(beta);
+    if (valid && hl == 0) {
+      s_cnt[gg][wave][0] = dt;
+      s_cnt[gg][wave][1] = st;
+      s_bpart[gg][wave] = bs;
     }
-#pragma unroll
-    for (int q = 0; q < 2; ++q) {
-      if (q >= ns) break;
-      const bool ra = (q == 0) && nsa;
-      const int j = ra ? da : db;                             // the odd last plane
-      const uint32_t off = (uint32_t)((k0 + (ra ? 0 : 1)) * L.RB + (j - 1) * PLANE);
-      const int i = spos + q, u = pad_du + (i >> 2), sub = (i >> 1) & 1, h = i & 1;
-      U[u * 8 + 4 * sub + h] = off;
-      reinterpret_cast<uint16_t*>(&U[u * 8 + 4 * sub + 2])[h] = (uint16_t)((29 - 2 * j) << 10);
-      reinterpret_cast<uint16_t*>(&U[u * 8 + 4 * sub + 3])[h] = (uint16_t)(ra ? xa : xb);
-    }
-    // empty items up to whole batches: offset 0 (the tile's first row, in
-    // bounds), zero coefficient, a finite exponent word
-    for (int i = dtot + lane; i < 2 * pad_du; i += 64) {
-      const int u = i >> 1, h = i & 1;
-      U[u * 8 + h] = 0u;
-      U[u * 8 + 4 + h] = 0u;
-      reinterpret_cast<uint16_t*>(&U[u * 8 + 2])[h] = (uint16_t)(27 << 10);
-      reinterpret_cast<uint16_t*>(&U[u * 8 + 3])[h] = 0;
-    }
-    for (int i = stot + lane; i < 4 * pad_su; i += 64) {
-      const int u = pad_du + (i >> 2), sub = (i >> 1) & 1, h = i & 1;
-      U[u * 8 + 4 * sub + h] = 0u;
-      reinterpret_cast<uint16_t*>(&U[u * 8 + 4 * sub + 2])[h] = (uint16_t)(27 << 10);
-      reinterpret_cast<uint16_t*>(&U[u * 8 + 4 * sub + 3])[h] = 0;
-    }
-    const float bs = wave_sum_dpp(beta);
-    if (lane == 0) {
-      s_beta[gg] = bs;
-      s_nbd[gg] = pad_du / kSlots;
-      s_nb[gg] = (pad_du + pad_su) / kSlots;
-    }
+    if (sg) reinterpret_cast<uint16_t*>(s_spx)[row] = d ? (uint16_t)xv[i] : (uint16_t)0;
   }
   for (int i = tid; i < kSlots * 8; i += kThreads) {
     const int w = i % 8;
@@ -238,11 +218,84 @@ __global__ __launch_bounds__(kThreads) void k_vmm_pp(
   }
   __syncthreads();
 
+  // items at their places; padding and the per-group totals
+#pragma unroll
+  for (int i = 0; i < kPasses; ++i) {
+    if (i > 0 && 2 * i >= ng) break;
+    const int gg = 2 * i + half;
+    if (gg < ng) {
+      int dbase = 0, sbase = 0, dtot = 0, stot = 0;
+#pragma unroll
+      for (int w = 0; w < kWaves; ++w) {
+        const int a = s_cnt[gg][w][0], b = s_cnt[gg][w][1];
+        dbase += w < wave ? a : 0;
+        sbase += w < wave ? b : 0;
+        dtot += a;
+        stot += b;
+      }
+      const int n_du = (dtot + 1) >> 1, n_su = (stot + 3) >> 2;
+      const int pad_du = (n_du + kSlots - 1) / kSlots * kSlots;
+      int pad_su = (n_su + kSlots - 1) / kSlots * kSlots;
+      if (pad_du + pad_su == 0) pad_su = kSlots;   // an empty group still gets one batch
+      uint32_t* U = &s_units[gg][0][0];
+      const int k = (g0 + gg) * kGroup + row;
+      const uint32_t xh = xv[i] & 0xFFFFu;
+      const bool sg = SPEC && gg == 0;
+      const int j0 = sg ? 2 : 1;
+#pragma unroll
+      for (int q = 0; q < 2; ++q) {
+        if (q < ndb[i]) {
+          const int j = j0 + 2 * q;                           // first plane of the pair
+          const uint32_t off = (uint32_t)(k * L.RB + (j - 1) * PLANE);
+          const int it = dbase + dpos[i] + q, u = it >> 1, h = it & 1;
+          U[u * 8 + h] = off;
+          U[u * 8 + 4 + h] = off + PLANE;
+          reinterpret_cast<uint16_t*>(&U[u * 8 + 2])[h] = (uint16_t)((31 - 2 * j) << 10);
+          reinterpret_cast<uint16_t*>(&U[u * 8 + 3])[h] = (uint16_t)xh;
+        }
+      }
+      if (nsg[i]) {
+        const int j = dep[i];                                 // the last plane
+        const uint32_t off = (uint32_t)(k * L.RB + (j - 1) * PLANE);
+        const int it = sbase + spos[i], u = pad_du + (it >> 2), sub = (it >> 1) & 1, h = it & 1;
+        U[u * 8 + 4 * sub + h] = off;
+        reinterpret_cast<uint16_t*>(&U[u * 8 + 4 * sub + 2])[h] = (uint16_t)((29 - 2 * j) << 10);
+        reinterpret_cast<uint16_t*>(&U[u * 8 + 4 * sub + 3])[h] = (uint16_t)xh;
+      }
+      // empty items up to whole batches, spread over the group's 128 lanes:
+      // offset 0 (the tile's first row, in bounds), zero coefficient, a
+      // finite exponent word
+      const int pl = row;
+      for (int it = dtot + pl; it < 2 * pad_du; it += kGroup) {
+        const int u = it >> 1, h = it & 1;
+        U[u * 8 + h] = 0u;
+        U[u * 8 + 4 + h] = 0u;
+        reinterpret_cast<uint16_t*>(&U[u * 8 + 2])[h] = (uint16_t)(27 << 10);
+        reinterpret_cast<uint16_t*>(&U[u * 8 + 3])[h] = 0;
+      }
+      for (int it = stot + pl; it < 4 * pad_su; it += kGroup) {
+        const int u = pad_du + (it >> 2), sub = (it >> 1) & 1, h = it & 1;
+        U[u * 8 + 4 * sub + h] = 0u;
+        reinterpret_cast<uint16_t*>(&U[u * 8 + 4 * sub + 2])[h] = (uint16_t)(27 << 10);
+        reinterpret_cast<uint16_t*>(&U[u * 8 + 4 * sub + 3])[h] = 0;
+      }
+      if (row == 0) {
+        s_beta[gg] = s_bpart[gg][0] + s_bpart[gg][1] + s_bpart[gg][2] + s_bpart[gg][3];
+        s_nbd[gg] = pad_du / kSlots;
+        s_nb[gg] = (pad_du + pad_su) / kSlots;
+      }
+    }
+  }
+  // the scales come from HBM and arrive after x: stored last (a quarter of
+  // each group's per wave)
+#pragma unroll
+  for (int gg = 0; gg < kPPMaxGW; ++gg)
+    if (gg < ng) *(ScaleWord*)&s_scale[gg][(wave * 64 + lane) * SH] = scw[gg];
+  __syncthreads();
+
   // ---- main loop: lane group lg takes units lg, lg + kLaneGroups, ... of
   // each batch; the (group, batch) sequence runs through four register sets,
   // three batches in flight while one is consumed.
-  const uint8_t* tile = codes + (size_t)t * L.K * L.RB;
-  const uint32_t li4 = (uint32_t)li * 4u;
   float yp[16], acc[16], off_d = 0.0f, off_s = 0.0f;
 #pragma unroll
   for (int e = 0; e < 16; ++e) yp[e] = acc[e] = 0.0f;
@@ -343,6 +396,25 @@ __global__ __launch_bounds__(kThreads) void k_vmm_pp(
   Batch R[D];
 #pragma unroll
   for (int i = 0; i < D - 1; ++i) fetch(R[i], i);
+  if constexpr (SPEC) {
+    // the read-ahead plane-1 rows of the first group, as singles (exponent
+    // 29 - 2j at j = 1), while the first batches of the lists are in flight
+    constexpr uint32_t e1 = (27u << 10) | (27u << 26);
+    float a2[1][16];
+#pragma unroll
+    for (int e = 0; e < 16; ++e) a2[0][e] = acc[e];
+#pragma unroll
+    for (int q = 0; q < kSpecPerLG; ++q) {
+      const int u = lg + kLaneGroups * q;
+      const uint32_t xp0[1] = {s_spx[2 * u]}, xp1[1] = {s_spx[2 * u + 1]};
+      off_s = dot2(e1, xp0[0], off_s);
+      off_s = dot2(e1, xp1[0], off_s);
+      consume_pair<1, 16>(spw[4 * q], spw[4 * q + 1], e1, xp0, a2, 0);
+      consume_pair<1, 16>(spw[4 * q + 2], spw[4 * q + 3], e1, xp1, a2, 0);
+    }
+#pragma unroll
+    for (int e = 0; e < 16; ++e) acc[e] = a2[0][e];
+  }
   for (int b = 0; b < nbt; b += D) {
 #pragma unroll
     for (int i = 0; i < D; ++i) {
@@ -370,15 +442,29 @@ loop_done:
     for (int w = 0; w < kWaves; ++w) v += s_red[w][o];
     atomicAdd(&y[(size_t)t * T + o], v * L.sfac);   // 8-bit code units -> b_max units
   }
-  if constexpr (PREFETCH) asm volatile("s_waitcnt vmcnt(0)" : "+v"(pf)::"memory");
 }
 
 template <int LPR>
 void launch_pp(dim3 grid, hipStream_t s, const void* codes, const void* scales, const void* x,
                const uint8_t* lm, float* y, const Layer& L, int gw, int fused,
                const Thresholds& th, uint8_t* lm_out) {
-  hipLaunchKernelGGL((k_vmm_pp<LPR, 2, GRINQH_PP_DEPTH, 256, GRINQH_PP_PREFETCH>), grid, dim3(256), 0, s, (const uint8_t*)codes,
-                     (const uint16_t*)scales, (const uint16_t*)x, lm, y, L, gw, fused, th, lm_out);
+  // Plane-1 read-ahead pays where a CU holds about one workgroup, whose own
+  // prologue is then the only thing to hide the first loads behind; with
+  // more workgroups per CU the others hide it, and the read-ahead's level-0
+  // rows only cost bandwidth.  GRINQH_VMM_SPEC=0/1 forces it.
+  static const int forced = [] {
+    const char* e = getenv("GRINQH_VMM_SPEC");
+    return e ? atoi(e) : -1;
+  }();
+  const bool spec = forced >= 0 ? forced != 0 : grid.x <= 384;
+  if (spec)
+    hipLaunchKernelGGL((k_vmm_pp<LPR, 2, GRINQH_PP_DEPTH, 256, true>), grid, dim3(256), 0, s,
+                       (const uint8_t*)codes, (const uint16_t*)scales, (const uint16_t*)x, lm, y, L, gw, fused,
+                       th, lm_out);
+  else
+    hipLaunchKernelGGL((k_vmm_pp<LPR, 2, GRINQH_PP_DEPTH, 256, false>), grid, dim3(256), 0, s,
+                       (const uint8_t*)codes, (const uint16_t*)scales, (const uint16_t*)x, lm, y, L, gw, fused,
+                       th, lm_out);
 }
 
 }  // namespace
