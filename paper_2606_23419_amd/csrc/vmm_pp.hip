@@ -452,11 +452,8 @@ void launch_pp(dim3 grid, hipStream_t s, const void* codes, const void* scales, 
   // prologue is then the only thing to hide the first loads behind; with
   // more workgroups per CU the others hide it, and the read-ahead's level-0
   // rows only cost bandwidth.  GRINQH_VMM_SPEC=0/1 forces it.
-  static const int forced = [] {
-    const char* e = getenv("GRINQH_VMM_SPEC");
-    return e ? atoi(e) : -1;
-  }();
-  const bool spec = forced >= 0 ? forced != 0 : grid.x <= 384;
+  const char* forced = getenv("GRINQH_VMM_SPEC");
+  const bool spec = forced ? atoi(forced) != 0 : grid.x <= 384;
   if (spec)
     hipLaunchKernelGGL((k_vmm_pp<LPR, 2, GRINQH_PP_DEPTH, 256, true>), grid, dim3(256), 0, s,
                        (const uint8_t*)codes, (const uint16_t*)scales, (const uint16_t*)x, lm, y, L, gw, fused,

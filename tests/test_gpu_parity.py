@@ -347,6 +347,39 @@ def test_vmm_groups_per_workgroup(g, torch, gw, tile_n, kernel, monkeypatch):
         assert normwise(y, ref) <= TOL, (gw, tile_n, B, normwise(y, ref))
 
 
+@pytest.mark.parametrize("spec", ["0", "1"])
+@pytest.mark.parametrize("gw", ["1", "2", "3", "4"])
+@pytest.mark.parametrize("tile_n", [256, 512, 1024])
+@pytest.mark.parametrize("levels", [(0, 2, 4, 6, 8), (0, 2, 4, 6), (0, 2, 4)])
+def test_vmm_plane1_readahead(g, torch, spec, gw, tile_n, levels, monkeypatch):
+    # The batch-1 plane-pair kernel with the plane-1 read-ahead forced on or
+    # off, for every groups-per-workgroup count (only the first group of a
+    # workgroup is read ahead), b_max 8, 6 and 4, through the level-map and
+    # the fused-threshold entry points.  K = 1152 is 9 groups: ragged last
+    # workgroups for gw > 1.
+    monkeypatch.setenv("GRINQH_VMM_SPEC", spec)
+    monkeypatch.setenv("GRINQH_VMM_GW", gw)
+    K, N = 1152, 1024
+    L = Layer(g, torch, K, N, levels, cfg=69, tile_n=tile_n)
+    rng = np.random.default_rng(69)
+    n = len(levels)
+    lm = rng.integers(0, n, size=(1, K)).astype(np.uint8)
+    lm[0, :128] = 0                            # a first group with nothing to read
+    lm[0, 256:384] = n - 1                     # and one at full depth
+    x = inputs.activations_t3(K, 1, 69, int(spec) * 16 + int(gw))
+    y, ref = _vmm_case(g, torch, L, x, lm)
+    assert normwise(y, ref) <= TOL, (spec, gw, tile_n, levels, normwise(y, ref))
+    # fused grading: thresholds at quantiles of |x|, level map written out
+    ax = np.sort(np.abs(x[0].astype(np.float32)))
+    th = ax[np.linspace(0, K - 1, n + 1).astype(int)[1:-1]]
+    lm_out = torch.zeros((1, K), dtype=torch.uint8, device="cuda")
+    yt = g.grinqh_vmm_threshold(L.desc, L.pc, L.ps, _dev(torch, x), th, level_map_out=lm_out)
+    torch.cuda.synchronize()
+    lmt = orc.assign_threshold(x, th)
+    assert np.array_equal(_host(lm_out), lmt)
+    assert normwise(_host(yt), orc.vmm_batch(L.codes, L.scales, x, lmt, levels)) <= TOL
+
+
 @pytest.mark.parametrize("kernel", ["pp", "dot2"])
 def test_vmm_precision_margin(g, torch, kernel, monkeypatch):
     # the contract is 1e-3; the fp32 accumulation should sit far below it
