@@ -26,6 +26,7 @@
 //   beta_g = sum_{k: level > 0} x_k (phi_b - 128)  (midpoint bias, offset),
 // which equals sum_k x_k s (t_k + phi - 128) with t_k the truncated code.
 #include <cstdlib>
+#include <type_traits>
 
 #include "grinqh_internal.h"
 #include "vmm_common.h"
@@ -66,6 +67,8 @@ __global__ __launch_bounds__(kThreads) void k_vmm_dot2(
   __shared__ float s_beta[max_gw(NB)][NB];
   __shared__ __align__(16) uint16_t s_scale[max_gw(NB)][T];
   __shared__ __align__(16) float s_red[NB][kWaves][T];
+  __shared__ int s_cnt[max_gw(NB)][kWaves][2];         // full pairs, lone items per group and wave
+  __shared__ float s_bpart[max_gw(NB)][NB][kWaves];    // beta_g partial sums per wave
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int t = blockIdx.x % L.tiles;
@@ -75,127 +78,179 @@ __global__ __launch_bounds__(kThreads) void k_vmm_dot2(
   const int lg = tid / LPR, li = tid % LPR;
 
 
-  // ---- prologue: one wave per group.  Lane l grades rows 2l and 2l+1, lists
-  // their plane rows (row 2l first, planes in order) and pairs them in order;
-  // a pair's second slot is empty when the lane's count is odd.  Pair slots
-  // are placed by ballot prefix counts, so the lane writes its descriptors
-  // straight into the group's list.
-  for (int gg = wave; gg < ng; gg += kWaves) {
-    const int g = g0 + gg;
-    const int r0 = 2 * lane;
-    const int k0 = g * kGroup + r0;
-    // x, the level map and the scales are requested together, so the
-    // prologue waits for one memory latency, not two
-    uint32_t xxs[NB];
-    uint16_t lls[NB];
-    const uint8_t* lmsrc = fused ? (const uint8_t*)x : lm;   // in fused mode the read is ignored
+  // ---- prologue.  The four waves grade the rows together: in pass i, lane
+  // l of wave w takes row 32w + (l & 31) of group 2i + (l >> 5), so each half
+  // wave covers 32 rows of one group.  A lane lists its row's plane rows
+  // 1..D (D the deepest over the tokens) as the pairs (1,2), (3,4), ...; a
+  // last odd plane is a lone item, and the group's lone items are paired
+  // with each other after all full pairs (the second slot of an odd last one
+  // repeats the first with zero coefficients).  A half wave's items follow
+  // those of the lower waves' halves of the same group, whose counts are
+  // exchanged through LDS.
+  static_assert(kWaves == 4 && kGroup == 128, "32 rows per half wave");
+  constexpr int kPasses = (max_gw(NB) + 1) / 2;
+  constexpr int SH = T / 256;                // scale halves per lane and group
+  constexpr int kMaxPlanes = 8 / U;
+  const int half = lane >> 5, hl = lane & 31;
+  const int row = 32 * wave + hl;            // row of the group
+  // x, the level map and the scales are requested together, and
+  // unconditionally (groups past the workgroup's last one read that one
+  // again, from cache), so the compiler waits for x alone before grading
+  uint32_t xv[kPasses][NB], lv[kPasses][NB];
+  using ScaleWord = typename std::conditional<SH == 4, uint2, typename std::conditional<SH == 2, uint32_t, uint16_t>::type>::type;
+  ScaleWord scw[max_gw(NB)];
+  const uint8_t* lmsrc = fused ? (const uint8_t*)x : lm;   // in fused mode the read is ignored
+#pragma unroll
+  for (int i = 0; i < kPasses; ++i) {
+    const int k = (g0 + min(2 * i + half, ng - 1)) * kGroup + row;
 #pragma unroll
     for (int b = 0; b < NB; ++b) {
-      xxs[b] = *(const uint32_t*)(x + (size_t)b * L.K + k0);
-      lls[b] = *(const uint16_t*)(lmsrc + (size_t)b * L.K + k0);
+      xv[i][b] = x[(size_t)b * L.K + k];
+      lv[i][b] = lmsrc[(size_t)b * L.K + k];
     }
-    {   // this group's scales for the tile go to LDS: T fp16 = 64 lanes x 4V halves
-      constexpr int H = T / 64;   // halves per lane: 4, 8 or 16
-      const uint16_t* sp = scales + (size_t)g * L.N + (size_t)t * T + lane * H;
-      if constexpr (H == 4) {
-        *(uint2*)&s_scale[gg][lane * H] = *(const uint2*)sp;
-      } else {
+  }
 #pragma unroll
-        for (int c = 0; c < H / 8; ++c) *(uint4*)&s_scale[gg][lane * H + 8 * c] = *(const uint4*)(sp + 8 * c);
-      }
-    }
+  for (int gg = 0; gg < max_gw(NB); ++gg)
+    scw[gg] = *(const ScaleWord*)(scales + (size_t)(g0 + min(gg, ng - 1)) * L.N + (size_t)t * T +
+                                  (wave * 64 + lane) * SH);
+  __builtin_amdgcn_sched_barrier(0);
+
+  // grade, count pairs, local positions
+  int dtok[kPasses][NB], dmax[kPasses], ppos[kPasses], lpos[kPasses];
 #pragma unroll
-    for (int b = 0; b < NB; ++b) asm volatile("" ::"v"(lls[b]));   // level-map loads issued before the wait above
-    int da[NB], db[NB];
-    int D0 = 0, D1 = 0;
-    float beta[NB];
+  for (int i = 0; i < kPasses; ++i) {
+    if (i > 0 && 2 * i >= ng) break;         // uniform: the groups of this pass are absent
+    const int gg = 2 * i + half;
+    const bool valid = gg < ng;
+    int D = 0;
 #pragma unroll
     for (int b = 0; b < NB; ++b) {
-      const float fa = h2f((uint16_t)(xxs[b] & 0xFFFFu)), fb = h2f((uint16_t)(xxs[b] >> 16));
-      int la, lb;
-      if (fused) {
-        la = 0;
-        lb = 0;
-        const float aa = fabsf(fa), ab = fabsf(fb);
+      const float fx = h2f((uint16_t)xv[i][b]);
+      // graded from x (th.n is 0 without thresholds) or read from the level
+      // map, chosen without a branch so that the level-map load stays early
+      int graded = 0;
+      const float ax = fabsf(fx);
 #pragma unroll
-        for (int j = 0; j < kMaxLevels - 1; ++j) {   // unrolled: the thresholds are one scalar load
-          la += (j < th.n && aa >= th.theta[j]) ? 1 : 0;
-          lb += (j < th.n && ab >= th.theta[j]) ? 1 : 0;
-        }
-        if (lm_out && t == 0)
-          *(uint16_t*)(lm_out + (size_t)b * L.K + k0) = (uint16_t)(la | (lb << 8));
-      } else {
-        la = min((int)(lls[b] & 0xFFu), n_top);
-        lb = min((int)(lls[b] >> 8), n_top);
+      for (int j = 0; j < kMaxLevels - 1; ++j) {
+        if (j >= th.n) break;                // uniform
+        graded += ax >= th.theta[j] ? 1 : 0;
       }
-      da[b] = level_planes(L.planes_packed, la);
-      db[b] = level_planes(L.planes_packed, lb);
-      D0 = max(D0, da[b]);
-      D1 = max(D1, db[b]);
-      beta[b] = (la ? fa * phi_minus_offset(U * da[b], L.bmax) : 0.0f) +
-                (lb ? fb * phi_minus_offset(U * db[b], L.bmax) : 0.0f);
+      const int lvl = fused ? graded : min((int)(lv[i][b] & 0xFFu), n_top);
+      if (fused && lm_out && t == 0 && valid) lm_out[(size_t)b * L.K + (g0 + gg) * kGroup + row] = (uint8_t)lvl;
+      const int d = valid ? level_planes(L.planes_packed, lvl) : 0;
+      dtok[i][b] = d;
+      D = max(D, d);
+      const float bs = half_sum_dpp(d ? fx * phi_minus_offset(U * d, L.bmax) : 0.0f);
+      if (valid && hl == 0) s_bpart[gg][b][wave] = bs;
     }
-    const int cnt = D0 + D1;
-    const int np = (cnt + 1) >> 1;
-    int pos = 0, total = 0;
+    dmax[i] = D;
+    const int np = D >> 1;                   // full pairs
+    int pos = 0, tot = 0;
 #pragma unroll
-    for (int q = 1; q <= 8 / U; ++q) {
-      pos += lanes_below(np >= q);
-      total += lanes_total(np >= q);
+    for (int q = 1; q <= kMaxPlanes / 2; ++q) {
+      pos += half_below(np >= q);
+      tot += half_total(np >= q);
     }
+    ppos[i] = pos;
+    lpos[i] = half_below(D & 1);
+    const int ltot = half_total(D & 1);
+    if (valid && hl == 0) {
+      s_cnt[gg][wave][0] = tot;
+      s_cnt[gg][wave][1] = ltot;
+    }
+  }
+  for (int i = tid; i < (kThreads / LPR * PB) * DW; i += kThreads)
+    (&s_empty[0][0])[i] = (i % DW == 2) ? ((27u << 10) | (27u << 26)) : 0u;
+  __syncthreads();
+
+  // pairs at their places; padding and the per-group totals
 #pragma unroll
-    for (int q = 0; q < 8 / U; ++q) {
-      if (2 * q >= cnt) break;
-      // items 2q and 2q+1 of the lane: item i is (row r0, plane i+1) below D0,
-      // else (row r0+1, plane i-D0+1)
-      const int ia = 2 * q, ib = 2 * q + 1;
-      const bool has_b = ib < cnt;
-      const int ra = ia < D0 ? 0 : 1, ja = ia < D0 ? ia + 1 : ia - D0 + 1;
-      const int rb = ib < D0 ? 0 : 1, jb = has_b ? (ib < D0 ? ib + 1 : ib - D0 + 1) : ja;
-      const int rbb = has_b ? rb : ra;
-      uint32_t* d = s_pairs[gg][pos + q];
+  for (int i = 0; i < kPasses; ++i) {
+    if (i > 0 && 2 * i >= ng) break;
+    const int gg = 2 * i + half;
+    if (gg < ng) {
+      int base = 0, ftot = 0, lbase = 0, ltot = 0;
+#pragma unroll
+      for (int w = 0; w < kWaves; ++w) {
+        const int c = s_cnt[gg][w][0], l = s_cnt[gg][w][1];
+        base += w < wave ? c : 0;
+        ftot += c;
+        lbase += w < wave ? l : 0;
+        ltot += l;
+      }
+      const int total = ftot + ((ltot + 1) >> 1);
+      const int k = (g0 + gg) * kGroup + row;
+      const int D = dmax[i];
       // plane j of width U is worth 2^(8 - U j) code units: exponent base 29 - U j
-      d[0] = (uint32_t)((k0 + ra) * L.RB + (ja - 1) * (T * U / 8));
-      d[1] = (uint32_t)((k0 + rbb) * L.RB + (jb - 1) * (T * U / 8));
-      d[2] = ((uint32_t)(29 - U * ja) << 10) | ((uint32_t)(29 - U * jb) << 26);
 #pragma unroll
-      for (int b = 0; b < NB; ++b) {
-        const uint32_t xa = ra ? (xxs[b] >> 16) : (xxs[b] & 0xFFFFu);
-        const uint32_t xb = rb ? (xxs[b] >> 16) : (xxs[b] & 0xFFFFu);
-        const int dA = ra ? db[b] : da[b];
-        const int dB = rb ? db[b] : da[b];
-        const uint32_t c1 = ja <= dA ? xa : 0u;
-        const uint32_t c2 = (has_b && jb <= dB) ? xb : 0u;
-        d[3 + b] = c1 | (c2 << 16);
+      for (int q = 0; q < kMaxPlanes / 2; ++q) {
+        if (2 * q + 2 > D) break;
+        const int ja = 2 * q + 1, jb = ja + 1;
+        uint32_t* d = s_pairs[gg][base + ppos[i] + q];
+        d[0] = (uint32_t)(k * L.RB + (ja - 1) * (T * U / 8));
+        d[1] = (uint32_t)(k * L.RB + (jb - 1) * (T * U / 8));
+        d[2] = ((uint32_t)(29 - U * ja) << 10) | ((uint32_t)(29 - U * jb) << 26);
+#pragma unroll
+        for (int b = 0; b < NB; ++b) {
+          const uint32_t xt = xv[i][b] & 0xFFFFu;
+          const uint32_t c1 = ja <= dtok[i][b] ? xt : 0u;
+          const uint32_t c2 = jb <= dtok[i][b] ? xt : 0u;
+          d[3 + b] = c1 | (c2 << 16);
+        }
+#pragma unroll
+        for (int w = 3 + NB; w < DW; ++w) d[w] = 0u;
       }
+      if (D & 1) {
+        // lone item li of the group: pair ftot + li/2, slot li%2 (16-bit
+        // halves of the exponent and coefficient words)
+        const int j = D;
+        const int it = lbase + lpos[i], slot = it & 1;
+        uint32_t* d = s_pairs[gg][ftot + (it >> 1)];
+        const uint32_t off = (uint32_t)(k * L.RB + (j - 1) * (T * U / 8));
+        const uint16_t ex = (uint16_t)((29 - U * j) << 10);
+        d[slot] = off;
+        reinterpret_cast<uint16_t*>(&d[2])[slot] = ex;
 #pragma unroll
-      for (int w = 3 + NB; w < DW; ++w) d[w] = 0u;
-    }
+        for (int b = 0; b < NB; ++b)
+          reinterpret_cast<uint16_t*>(&d[3 + b])[slot] = j <= dtok[i][b] ? (uint16_t)xv[i][b] : (uint16_t)0;
+        if (slot == 0) {
 #pragma unroll
-    for (int b = 0; b < NB; ++b) {
-      const float bs = wave_sum_dpp(beta[b]);
-      if (lane == 0) s_beta[gg][b] = bs;
-    }
-    // pad the list to whole batches with empty descriptors (zero coefficients,
-    // offset 0, a finite exponent word), so the main loop needs no bounds tests
-    {
-      // an empty list still gets one batch (its group epilogue runs), so it
-      // is padded to kSlots, never to 0
+          for (int w = 3 + NB; w < DW; ++w) d[w] = 0u;
+          if (it == ltot - 1) {   // odd count: the last pair's second slot repeats this one, zero coefficients
+            d[1] = off;
+            reinterpret_cast<uint16_t*>(&d[2])[1] = ex;
+#pragma unroll
+            for (int b = 0; b < NB; ++b) reinterpret_cast<uint16_t*>(&d[3 + b])[1] = 0;
+          }
+        }
+      }
+      // pad the list to whole batches with empty descriptors (zero
+      // coefficients, offset 0, a finite exponent word), spread over the
+      // group's 128 lanes, so the main loop needs no bounds tests; an empty
+      // list still gets one batch (its group epilogue runs)
       constexpr int kSlots = kThreads / LPR * PB;
       const int padded = total > 0 ? (total + kSlots - 1) / kSlots * kSlots : kSlots;
-      for (int i = total + lane; i < padded; i += 64) {
-        uint32_t* d = s_pairs[gg][i];
+      for (int it = total + row; it < padded; it += kGroup) {
+        uint32_t* d = s_pairs[gg][it];
         d[0] = 0u;
         d[1] = 0u;
         d[2] = (27u << 10) | (27u << 26);
 #pragma unroll
         for (int w = 3; w < DW; ++w) d[w] = 0u;
       }
+      if (row == 0) {
+        s_npairs[gg] = total;
+#pragma unroll
+        for (int b = 0; b < NB; ++b)
+          s_beta[gg][b] = s_bpart[gg][b][0] + s_bpart[gg][b][1] + s_bpart[gg][b][2] + s_bpart[gg][b][3];
+      }
     }
-    if (lane == 0) s_npairs[gg] = total;
   }
-  for (int i = tid; i < (kThreads / LPR * PB) * DW; i += kThreads)
-    (&s_empty[0][0])[i] = (i % DW == 2) ? ((27u << 10) | (27u << 26)) : 0u;
+  // the scales come from HBM and arrive after x: stored last (a quarter of
+  // each group's per wave)
+#pragma unroll
+  for (int gg = 0; gg < max_gw(NB); ++gg)
+    if (gg < ng) *(ScaleWord*)&s_scale[gg][(wave * 64 + lane) * SH] = scw[gg];
   __syncthreads();
 
   // ---- main loop: lane group lg takes pairs lg, lg + 16, ... of every group.
@@ -402,14 +457,6 @@ int launch_vmm_dot2(const Layer& L, const void* codes, const void* scales, const
   Thresholds none{};
   const Thresholds& tt = th ? *th : none;
   const int fused = th != nullptr;
-  const char* env_nt = getenv("GRINQH_VMM_THREADS");
-  const int nt = (env_nt && atoi(env_nt) == 512 && B == 1) ? 512 : 256;
-  if (nt == 512 && L.u == 2) {
-    if (L.T == 256) launch_one<2, 1, 16, 1, 512>(grid, s, codes, scales, x, level_map, y, L, gw, fused, tt, level_map_out);
-    else if (L.T == 512) launch_one<2, 1, 32, 1, 512>(grid, s, codes, scales, x, level_map, y, L, gw, fused, tt, level_map_out);
-    else launch_one<2, 1, 64, 1, 512>(grid, s, codes, scales, x, level_map, y, L, gw, fused, tt, level_map_out);
-    return check_launch("vmm (dot2)");
-  }
 #define GRINQH_DOT2_CASE(UU, TT, LL, NN)                                                          \
   if (L.u == UU && L.T == TT && B == NN) {                                                       \
     launch_one<UU, 1, LL, NN, 256>(grid, s, codes, scales, x, level_map, y, L, gw, fused, tt, level_map_out); \

@@ -326,16 +326,15 @@ def test_full_size_pack_and_sampled_vmm(g, torch, name, K, N, levels, xkind):
         assert np.all(np.isfinite(y))
 
 
-@pytest.mark.parametrize("kernel", ["pp", "dot2-256", "dot2-512"])
+@pytest.mark.parametrize("kernel", ["pp", "dot2"])
 @pytest.mark.parametrize("gw", ["1", "2", "3", "4"])
 @pytest.mark.parametrize("tile_n", [256, 512, 1024])
 def test_vmm_groups_per_workgroup(g, torch, gw, tile_n, kernel, monkeypatch):
     # K = 1152 is 9 groups: every gw > 1 leaves a ragged last workgroup.  At
     # B = 1 the plane-pair kernel runs unless the per-plane kernel is forced.
     monkeypatch.setenv("GRINQH_VMM_GW", gw)
-    if kernel.startswith("dot2"):
+    if kernel == "dot2":
         monkeypatch.setenv("GRINQH_VMM_KERNEL", "dot2")
-        monkeypatch.setenv("GRINQH_VMM_THREADS", kernel.split("-")[1])
     levels = (0, 2, 4, 6, 8)
     K, N = 1152, 1024
     L = Layer(g, torch, K, N, levels, cfg=64, tile_n=tile_n)
