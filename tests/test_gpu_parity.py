@@ -379,6 +379,38 @@ def test_vmm_plane1_readahead(g, torch, spec, gw, tile_n, levels, monkeypatch):
     assert normwise(_host(yt), orc.vmm_batch(L.codes, L.scales, x, lmt, levels)) <= TOL
 
 
+@pytest.mark.parametrize("gw", ["1", "2", "3", "4"])
+@pytest.mark.parametrize("levels,tile_n", [((0, 2, 4, 6, 8), 256), ((0, 2, 4, 6, 8), 512),
+                                           ((0, 2, 4, 6, 8), 1024), ((0, 2, 4, 6), 512),
+                                           ((0, 2, 3, 4, 8), 512), ((0, 2, 3, 4, 8), 1024)])
+def test_vmm_per_plane_depth_mix(g, torch, gw, levels, tile_n, monkeypatch):
+    # The per-plane kernel (batches, 1-bit planes, and 2-bit planes at B = 1
+    # when forced): per-token depths, lone last planes paired across rows
+    # (odd and even counts of them), ragged workgroups (K = 1152), through
+    # the level-map and the fused-threshold entry points.
+    monkeypatch.setenv("GRINQH_VMM_GW", gw)
+    monkeypatch.setenv("GRINQH_VMM_KERNEL", "dot2")
+    K, N = 1152, 1024
+    L = Layer(g, torch, K, N, levels, cfg=71, tile_n=tile_n)
+    rng = np.random.default_rng(71)
+    n = len(levels)
+    for B in (1, 2, 4):
+        lm = rng.integers(0, n, size=(B, K)).astype(np.uint8)
+        lm[:, :128] = 0                        # a first group with nothing to read
+        lm[0, 128:256] = n - 1                 # one token at full depth in the next
+        x = inputs.activations_t3(K, B, 71, B)
+        y, ref = _vmm_case(g, torch, L, x, lm)
+        assert normwise(y, ref) <= TOL, (gw, levels, tile_n, B, normwise(y, ref))
+        ax = np.sort(np.abs(x.astype(np.float32)).ravel())
+        th = ax[np.linspace(0, ax.size - 1, n + 1).astype(int)[1:-1]]
+        lm_out = torch.zeros((B, K), dtype=torch.uint8, device="cuda")
+        yt = g.grinqh_vmm_threshold(L.desc, L.pc, L.ps, _dev(torch, x), th, level_map_out=lm_out)
+        torch.cuda.synchronize()
+        lmt = orc.assign_threshold(x, th)
+        assert np.array_equal(_host(lm_out), lmt)
+        assert normwise(_host(yt), orc.vmm_batch(L.codes, L.scales, x, lmt, levels)) <= TOL, (gw, B)
+
+
 @pytest.mark.parametrize("kernel", ["pp", "dot2"])
 def test_vmm_precision_margin(g, torch, kernel, monkeypatch):
     # the contract is 1e-3; the fp32 accumulation should sit far below it
