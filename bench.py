@@ -22,7 +22,9 @@ Output: one JSON line.  `value` is whole-step throughput in GB/s of required
 bytes (sum over every VMM of the bytes its level map requires: code prefixes,
 scales of groups with an active channel, x, y, and the level map where one is
 read); `roofline` is for the VMM kernel alone, timed with HIP events on its
-own stream.
+own stream.  `vs_bits` repeats the VMM-only timing at every average-bit
+budget of the level set (thresholds calibrated per budget): µs per VMM, GB/s
+of required bytes and the fraction of the HBM peak against average bits.
 """
 from __future__ import annotations
 
@@ -168,6 +170,8 @@ def parse():
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
     ap.add_argument("--vmm-only-reps", type=int, default=5)
     ap.add_argument("--no-ref", action="store_true", help="skip the reference-shape timings")
+    ap.add_argument("--no-bits-sweep", action="store_true",
+                    help="skip the per-budget timings (vs_bits) of the default workload")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain copy of MIB MiB (counter calibration) and exit")
     ap.add_argument("--vmm-source-sha", action="store_true",
@@ -754,6 +758,30 @@ def main():
         per_layer[name] = {"K": K, "N": N, "us_per_vmm": round(us, 3), "required_bytes": int(mean_req),
                            "GBps": round(mean_req / (us * 1e-6) / 1e9, 1), "tile_n": int(descs[name].tile_n)}
         del lg
+    # ---- time against average bits: the same step's VMM launches at every
+    # budget of the level set (thresholds calibrated per budget), timed the
+    # same way as us_per_vmm
+    vs_bits = {}
+    if main_mode == "threshold" and not args.no_bits_sweep:
+        saved = dict(thresholds)
+        for bb, pb in inputs.BUDGETS[levels].items():
+            for xin in range(n_inputs):
+                thresholds[xin] = g.grinqh_calibrate(desc_of_input[xin], calib[xin], pb).cpu().numpy()
+            with torch.cuda.stream(s):
+                step("threshold")                 # eager: writes this budget's level maps
+            torch.cuda.synchronize()
+            lmh = {xin: m.cpu().numpy() for xin, m in lm["threshold"].items()}
+            sb = sum(int(bytes_required(lmh[xin], levels, K, N, False).sum()) for _, K, N, xin, _ in layers)
+            vg = capture(lambda: step("threshold", vmm_only=True))
+            us = time_graph(vg, args.vmm_only_reps) * 1e3 / n_vmm
+            del vg
+            gbs = sb / n_vmm / (us * 1e-6) / 1e9
+            vs_bits[str(bb)] = {"achieved_avg_bits": round(float(np.mean([np.asarray(levels)[m].mean()
+                                                                          for m in lmh.values()])), 3),
+                                "us_per_vmm": round(us, 3), "GBps": round(gbs, 1),
+                                "frac": round(gbs / HBM_PEAK_GBS, 4)}
+        thresholds.update(saved)
+
     # reference shapes (e.g. the unmerged q and k/v projections), same input
     for name, K, N in ([] if args.no_ref else wl["ref"]):
         xin = next(xi for _, k, _, xi, _ in layers if k == K)
@@ -813,6 +841,7 @@ def main():
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "traffic": stored_traffic(wl_name, budget, main_mode)},
         "algorithmic_bytes_per_vmm": round(bytes_per_vmm, 1),
+        "vs_bits": vs_bits,
         "other_assignment": {
             "assignment": other, "ms_per_step": round(results[other]["ms_step"], 4),
             "value": round(results[other]["step_bytes"] / (results[other]["ms_step"] * 1e-3) / 1e9, 2),
