@@ -443,9 +443,12 @@ int vmm_dot2_groups_per_wg(const Layer& L) {
     const int v = atoi(env);
     if (v >= 1 && v <= kMaxGW) return v;
   }
-  // about two workgroups per CU when the layer has that many (tile, group) units
+  // about 512 workgroups (two per CU) when the layer has that many (tile,
+  // group) units: rounded to the nearest count for 2-bit planes, down for
+  // 1-bit planes (measured: decode B = 2, 4 at 896 units -4 to -10% with 2
+  // groups; Qwen3 gate|up, 768 units of 1-bit planes, +20% with 2)
   const long units = (long)L.tiles * L.groups;
-  int gw = (int)(units / 512);
+  int gw = (int)((units + (L.u == 2 ? 256 : 0)) / 512);
   return gw < 1 ? 1 : (gw > kMaxGW ? kMaxGW : gw);
 }
 
