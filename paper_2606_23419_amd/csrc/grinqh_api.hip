@@ -58,10 +58,12 @@ static int resolve(const grinqh_layer_desc* d, Layer* L, grinqh_layer_desc* out)
   if (T == 0) {
     // Auto: the widest tile (fewer, longer rows per workgroup) that still
     // leaves at least 256 (tile, group) work units for 256 CUs; if none does,
-    // the tile giving the most units.
+    // the tile giving the most units.  1-bit planes take 512 first: their
+    // 64-byte plane rows pair up in 128-byte lines, and every Qwen3-8B layer
+    // measured faster at 512 than at 1024.
     const long groups = d->K / kGroup;
-    const int cand[] = {1024, 512, 256};
-    for (int c : cand) {
+    const int cand2[] = {1024, 512, 256}, cand1[] = {512, 1024, 256};
+    for (int c : (u == 1 ? cand1 : cand2)) {
       if (c * u >= 512 && d->N % c == 0 && (long)(d->N / c) * groups >= 256) { T = c; break; }
     }
     if (T == 0) {

@@ -443,12 +443,12 @@ int vmm_dot2_groups_per_wg(const Layer& L) {
     const int v = atoi(env);
     if (v >= 1 && v <= kMaxGW) return v;
   }
-  // about 512 workgroups (two per CU) when the layer has that many (tile,
-  // group) units: rounded to the nearest count for 2-bit planes, down for
-  // 1-bit planes (measured: decode B = 2, 4 at 896 units -4 to -10% with 2
-  // groups; Qwen3 gate|up, 768 units of 1-bit planes, +20% with 2)
+  // 2-bit planes: about 512 workgroups (two per CU), rounded to the nearest
+  // count (decode B = 2, 4 at 896 units: -4 to -10% with 2 groups).  1-bit
+  // planes: one group per workgroup below 1536 units (Qwen3-8B at T = 512:
+  // down, 768 units, 25% slower with 2; gate|up, 1536 units, best with 2).
   const long units = (long)L.tiles * L.groups;
-  int gw = (int)((units + (L.u == 2 ? 256 : 0)) / 512);
+  int gw = L.u == 2 ? (int)((units + 256) / 512) : (int)(units / 768);
   return gw < 1 ? 1 : (gw > kMaxGW ? kMaxGW : gw);
 }
 
