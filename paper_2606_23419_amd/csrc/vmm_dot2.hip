@@ -66,7 +66,9 @@ __global__ __launch_bounds__(kThreads) void k_vmm_dot2(
   __shared__ int s_npairs[max_gw(NB)];
   __shared__ float s_beta[max_gw(NB)][NB];
   __shared__ __align__(16) uint16_t s_scale[max_gw(NB)][T];
-  __shared__ __align__(16) float s_red[NB][kWaves][T];
+  // cross-wave sums, one token at a time (the buffer does not grow with the
+  // tokens, so neither does the workgroup's LDS)
+  __shared__ __align__(16) float s_red[kWaves][T];
   __shared__ int s_cnt[max_gw(NB)][kWaves][2];         // full pairs, lone items per group and wave
   __shared__ float s_bpart[max_gw(NB)][NB][kWaves];    // beta_g partial sums per wave
 
@@ -401,21 +403,22 @@ __global__ __launch_bounds__(kThreads) void k_vmm_dot2(
   for (int b = 0; b < NB; ++b)
 #pragma unroll
     for (int e = 0; e < NACC; ++e) yp[b][e] = lane_group_sum<LPR>(yp[b][e]);
-  if (lane < LPR) {
 #pragma unroll
-    for (int b = 0; b < NB; ++b)
+  for (int b = 0; b < NB; ++b) {
+    if (b > 0) __syncthreads();   // the previous token's sums are read
+    if (lane < LPR) {
 #pragma unroll
       for (int c = 0; c < NACC / 4; ++c)
-        *(float4*)&s_red[b][wave][li * NACC + 4 * c] =
+        *(float4*)&s_red[wave][li * NACC + 4 * c] =
             make_float4(yp[b][4 * c], yp[b][4 * c + 1], yp[b][4 * c + 2], yp[b][4 * c + 3]);
-  }
-  __syncthreads();
-  for (int i = tid; i < NB * T; i += kThreads) {
-    const int b = i / T, o = i % T;
-    float v = 0.0f;
+    }
+    __syncthreads();
+    for (int o = tid; o < T; o += kThreads) {
+      float v = 0.0f;
 #pragma unroll
-    for (int w = 0; w < kWaves; ++w) v += s_red[b][w][o];
-    atomicAdd(&y[(size_t)b * L.N + (size_t)t * T + o], v * L.sfac);   // 8-bit units -> b_max units
+      for (int w = 0; w < kWaves; ++w) v += s_red[w][o];
+      atomicAdd(&y[(size_t)b * L.N + (size_t)t * T + o], v * L.sfac);   // 8-bit units -> b_max units
+    }
   }
 }
 
