@@ -22,9 +22,10 @@ Output: one JSON line.  `value` is whole-step throughput in GB/s of required
 bytes (sum over every VMM of the bytes its level map requires: code prefixes,
 scales of groups with an active channel, x, y, and the level map where one is
 read); `roofline` is for the VMM kernel alone, timed with HIP events on its
-own stream.  `vs_bits` repeats the VMM-only timing at every average-bit
-budget of the level set (thresholds calibrated per budget): µs per VMM, GB/s
-of required bytes and the fraction of the HBM peak against average bits.
+own stream.  With --bits-sweep, `vs_bits` repeats the VMM-only timing at
+every average-bit budget of the level set (thresholds calibrated per budget):
+µs per VMM, GB/s of required bytes and the fraction of the HBM peak against
+average bits.
 """
 from __future__ import annotations
 
@@ -170,8 +171,9 @@ def parse():
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
     ap.add_argument("--vmm-only-reps", type=int, default=5)
     ap.add_argument("--no-ref", action="store_true", help="skip the reference-shape timings")
-    ap.add_argument("--no-bits-sweep", action="store_true",
-                    help="skip the per-budget timings (vs_bits) of the default workload")
+    ap.add_argument("--bits-sweep", action="store_true",
+                    help="also time the VMM launches at every budget of the level set (vs_bits); off by "
+                         "default so that a kernel trace of the default run covers the one workload")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain copy of MIB MiB (counter calibration) and exit")
     ap.add_argument("--vmm-source-sha", action="store_true",
@@ -762,7 +764,7 @@ def main():
     # budget of the level set (thresholds calibrated per budget), timed the
     # same way as us_per_vmm
     vs_bits = {}
-    if main_mode == "threshold" and not args.no_bits_sweep:
+    if main_mode == "threshold" and args.bits_sweep:
         saved = dict(thresholds)
         for bb, pb in inputs.BUDGETS[levels].items():
             for xin in range(n_inputs):
@@ -841,7 +843,7 @@ def main():
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "traffic": stored_traffic(wl_name, budget, main_mode)},
         "algorithmic_bytes_per_vmm": round(bytes_per_vmm, 1),
-        "vs_bits": vs_bits,
+        **({"vs_bits": vs_bits} if vs_bits else {}),
         "other_assignment": {
             "assignment": other, "ms_per_step": round(results[other]["ms_step"], 4),
             "value": round(results[other]["step_bytes"] / (results[other]["ms_step"] * 1e-3) / 1e9, 2),
