@@ -304,6 +304,9 @@ FULL = [
     ("cfg3 down 14336->4096", 14336, 4096, inputs.LEVELS_B, "swiglu"),
     ("cfg4 qkv 4096->6144", 4096, 6144, inputs.LEVELS_C, "t3"),
     ("cfg4 down 12288->4096", 12288, 4096, inputs.LEVELS_C, "swiglu"),
+    # the merged projections the benchmarks run (two groups per workgroup)
+    ("cfg3 gate|up 4096->28672", 4096, 28672, inputs.LEVELS_B, "t3"),
+    ("cfg4 gate|up 4096->24576", 4096, 24576, inputs.LEVELS_C, "t3"),
 ]
 
 
@@ -324,6 +327,26 @@ def test_full_size_pack_and_sampled_vmm(g, torch, name, K, N, levels, xkind):
         # sampled outputs against the oracle, and the whole vector's scale
         assert normwise(y[:, rows], ref) <= TOL, (name, p)
         assert np.all(np.isfinite(y))
+    # one token (the batch-1 plane-pair kernel), from the level map and with
+    # the grading fused in (thresholds at the last budget's cut points)
+    y1 = _host(g.grinqh_vmm(L.desc, L.pc, L.ps, _dev(torch, x[:1]), lm[:1]))
+    ref1 = orc.vmm_batch(L.codes[rows], L.scales[:, rows], x[:1], lm_h[:1], levels)
+    assert normwise(y1[:, rows], ref1) <= TOL, (name, "B=1")
+    ax = np.sort(np.abs(x[0].astype(np.float32)))[::-1]
+    n = len(levels)
+    th = np.sort(ax[np.linspace(K // 8, K - K // 8, n - 1).astype(int)]).astype(np.float32)
+    lm_out = torch.zeros((1, K), dtype=torch.uint8, device="cuda")
+    yt = _host(g.grinqh_vmm_threshold(L.desc, L.pc, L.ps, _dev(torch, x[:1]), th, level_map_out=lm_out))
+    lmt = orc.assign_threshold(x[:1], th)
+    assert np.array_equal(_host(lm_out), lmt)
+    reft = orc.vmm_batch(L.codes[rows], L.scales[:, rows], x[:1], lmt, levels)
+    assert normwise(yt[:, rows], reft) <= TOL, (name, "threshold B=1")
+    # four tokens at once (the batched kernel, per-token cross-wave sums)
+    x4 = gen(K, 4, 71, K + N)
+    lm4 = g.grinqh_assign(L.desc, _dev(torch, x4), g.GRINQH_ASSIGN_TOPK, counts=counts)
+    y4 = _host(g.grinqh_vmm(L.desc, L.pc, L.ps, _dev(torch, x4), lm4))
+    ref4 = orc.vmm_batch(L.codes[rows], L.scales[:, rows], x4, _host(lm4), levels)
+    assert normwise(y4[:, rows], ref4) <= TOL, (name, "B=4")
 
 
 @pytest.mark.parametrize("kernel", ["pp", "dot2"])
