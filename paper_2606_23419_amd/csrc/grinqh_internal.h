@@ -56,6 +56,7 @@ struct LutDesc {
   long offset[kMaxLevels];
   int cum[kMaxLevels];
   int entries;      // sum over levels >= 1 of 2^b_l
+  int quad_pad;     // LDS padding (entries) after each 16-output quad of a level's tables: 16 or 0
 };
 
 struct TopkCuts {

@@ -41,7 +41,7 @@ __global__ __launch_bounds__(kLutThreads) void k_vmm_lut(const uint8_t* __restri
   constexpr uint32_t MASK = (1u << U) - 1u;
   extern __shared__ __align__(16) uint16_t s_lut[];          // [levels][kSub][2^b]
   __shared__ float s_red[kLutThreads / 64][kSub];
-  __shared__ int s_cum[kMaxLevels];                           // level l's block starts at kSub * s_cum[l]
+  __shared__ int s_cum[kMaxLevels];                           // level l's block starts at s_cum[l]
   __shared__ uint8_t s_lv[kMaxRun];                           // levels of the run's channels
   __shared__ uint16_t s_x[kMaxRun];                           // x of the run's channels
 
@@ -62,14 +62,35 @@ __global__ __launch_bounds__(kLutThreads) void k_vmm_lut(const uint8_t* __restri
   const int g1 = min(g0 + groups_per_split, L.groups);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
 
-  if (tid < kMaxLevels) s_cum[tid] = D.cum[tid];
-  // tables of the 64 outputs: level l's block is kSub * 2^b entries at
-  // D.offset[l] + n0 * 2^b of the table array, copied in 16-byte pieces
+  // LDS layout: level l's block starts at kSub * cum[l] + 4 pad (l - 1)
+  // entries and holds the 64 outputs' tables as four quads of 16 outputs,
+  // quad c at c (16 * 2^b + pad): the pad of 16 entries (8 banks) puts the
+  // four quads a wave reads in one step on different banks (unpadded their
+  // starts are 128-byte multiples apart, the same banks for every b >= 2)
+  const int pad = D.quad_pad;
+  if (tid < kMaxLevels) s_cum[tid] = kSub * D.cum[tid] + 4 * pad * max(tid - 1, 0);
+  // tables of the 64 outputs: level l's are kSub * 2^b entries at
+  // D.offset[l] + n0 * 2^b of the table array, 8 * 2^b pieces of 16 bytes,
+  // copied quad by quad.  A thread issues eight loads before its eight
+  // stores: one L2 latency per eight pieces rather than one per piece.
   for (int l = 1; l < L.n_levels; ++l) {
-    const int e = 1 << L.bits[l];
-    const uint4* src = (const uint4*)(luts + D.offset[l] + (size_t)n0 * e);
-    uint4* dst = (uint4*)(s_lut + kSub * D.cum[l]);
-    for (int i = tid; i < kSub * e / 8; i += kLutThreads) dst[i] = src[i];
+    const int b = L.bits[l];
+    const int np = 8 << b, qn = 2 << b;      // pieces of the level, of a quad
+    const uint4* src = (const uint4*)(luts + D.offset[l] + ((size_t)n0 << b));
+    uint16_t* dst = s_lut + kSub * D.cum[l] + 4 * pad * (l - 1);
+    for (int i0 = 0; i0 < np; i0 += 8 * kLutThreads) {
+      uint4 v[8];
+#pragma unroll
+      for (int q = 0; q < 8; ++q) v[q] = src[min(i0 + tid + q * kLutThreads, np - 1)];
+      __builtin_amdgcn_sched_barrier(0);     // keep the eight loads ahead of the stores
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        // (past the last piece: the last piece again, the same value to the
+        // same place, so that neither loads nor stores are conditional)
+        const int i = min(i0 + tid + q * kLutThreads, np - 1);
+        *(uint4*)(dst + (i / qn) * ((16 << b) + pad) + 8 * (i % qn)) = v[q];
+      }
+    }
   }
   __syncthreads();
 
@@ -91,57 +112,65 @@ __global__ __launch_bounds__(kLutThreads) void k_vmm_lut(const uint8_t* __restri
 #pragma unroll
   for (int e = 0; e < 16; ++e) acc[e] = 0.0f;
 
-  // rows rs + 64 m, m = 0, 1, ...: the plane words of the next row are
-  // requested before the current row's lookups
+  // Rows rs + 64 m, m = 0, 1, ..., through a ring of four register sets:
+  // three rows' plane words are in flight while one row is looked up.  The
+  // loads are unconditional (planes past a row's depth read the tile's first
+  // row, which stays in cache, and are masked to zero when consumed), so the
+  // compiler counts them and waits for the row being consumed alone.
   constexpr int kWords = 8 / U;
+  constexpr int R = 4;
   const uint8_t* tile_codes = codes + (size_t)t * L.K * L.RB + col;
   auto fetch = [&](int i, uint32_t (&w)[kWords]) __attribute__((always_inline)) {
     const int d = i < nrows ? level_planes(L.planes_packed, s_lv[i]) : 0;
     const uint8_t* row = tile_codes + (size_t)(kr0 + min(i, nrows - 1)) * L.RB;
 #pragma unroll
     for (int j = 0; j < kWords; ++j) {
-      if (j < d) {
-        if constexpr (U == 2) w[j] = *(const uint32_t*)(row + (size_t)j * plane_bytes);
-        else w[j] = *(const uint16_t*)(row + (size_t)j * plane_bytes);
-      } else {
-        w[j] = 0u;
-      }
+      const uint8_t* a = j < d ? row + (size_t)j * plane_bytes : tile_codes;
+      if constexpr (U == 2) w[j] = __builtin_nontemporal_load((const uint32_t*)a);
+      else w[j] = __builtin_nontemporal_load((const uint16_t*)a);
     }
   };
-  uint32_t wa[kWords], wb[kWords];
-  fetch(rs, wa);
-  for (int i = rs; i < nrows; i += 64) {
-    fetch(i + 64, wb);
-    const int lvl = s_lv[i];
+  auto consume = [&](int i, const uint32_t (&wv)[kWords]) __attribute__((always_inline)) {
+    const int lvl = i < nrows ? (int)s_lv[i] : 0;
     if (lvl != 0) {
       const float xv = h2f(s_x[i]);
       const int d = level_planes(L.planes_packed, lvl);
       const int b = d * U;
       // the 16 outputs' codes left-aligned in 8 bits (planes past d are
       // zero): byte i of qw[r] is output 4 i + r; q_b is its top b bits
+      uint32_t m[kWords];
+#pragma unroll
+      for (int j = 0; j < kWords; ++j) m[j] = j < d ? wv[j] : 0u;
       uint32_t w[4];
       if constexpr (U == 2) {
 #pragma unroll
-        for (int j = 0; j < 4; ++j) w[j] = wa[j];
+        for (int j = 0; j < 4; ++j) w[j] = m[j];
       } else {
 #pragma unroll
         for (int j = 0; j < 4; ++j)
-          w[j] = (vmmdev::spread_bits(wa[2 * j]) << 1) | vmmdev::spread_bits(wa[2 * j + 1]);
+          w[j] = (vmmdev::spread_bits(m[2 * j]) << 1) | vmmdev::spread_bits(m[2 * j + 1]);
       }
       uint32_t qw[4];
       vmmdev::assemble_codes(w[0], w[1], w[2], w[3], qw);
       const int sh = 8 - b;
-      // the lane's outputs' rows of level lvl's table: output 16 c + e at
-      // (16 c + e) * 2^b
-      const uint16_t* tb = s_lut + kSub * s_cum[lvl] + ((16 * c) << b);
+      // the lane's outputs' table quad of level lvl: output 16 c + e at e * 2^b
+      const uint16_t* tb = s_lut + s_cum[lvl] + c * ((16 << b) + pad);
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
         const uint32_t q8 = (qw[e & 3] >> (8 * (e >> 2))) & 0xFFu;
         acc[e] = fmaf(xv, h2f(tb[(e << b) + (q8 >> sh)]), acc[e]);
       }
     }
+  };
+  uint32_t wr[R][kWords];
 #pragma unroll
-    for (int j = 0; j < kWords; ++j) wa[j] = wb[j];
+  for (int q = 0; q < R - 1; ++q) fetch(rs + 64 * q, wr[q]);
+  for (int i = rs; i < nrows; i += 64 * R) {
+#pragma unroll
+    for (int q = 0; q < R; ++q) {
+      fetch(i + 64 * (q + R - 1), wr[(q + R - 1) % R]);
+      consume(i + 64 * q, wr[q]);
+    }
   }
 
   // lanes with equal (lane & 3) hold the same outputs: sum over lane bits 2..5
@@ -177,6 +206,9 @@ int lut_desc(const Layer& L, LutDesc* D) {
     }
   }
   D->entries = cum;
+  // quad padding in LDS when it fits in 64 KB (see the kernel)
+  const size_t padded = (size_t)kSub * cum * 2 + (size_t)4 * 16 * (L.n_levels - 1) * 2;
+  D->quad_pad = padded <= 65536 ? 16 : 0;
   return GRINQH_OK;
 }
 
@@ -184,19 +216,21 @@ int launch_vmm_lut(const Layer& L, const void* codes, const void* luts, const vo
                    const uint8_t* level_map, int B, float* y, int accumulate, hipStream_t s) {
   LutDesc D;
   lut_desc(L, &D);
-  const size_t lds = (size_t)kSub * D.entries * 2;   // <= 64 * 510 * 2 bytes: levels are distinct widths <= 8
+  // <= 64 * 510 * 2 bytes (levels are distinct widths <= 8), plus the quad padding where it fits
+  const size_t lds = (size_t)kSub * D.entries * 2 + (size_t)4 * D.quad_pad * (L.n_levels - 1) * 2;
   if (lds > 65536) return fail(GRINQH_EUNSUPPORTED, "LUT VMM: %d table entries per output", D.entries);
   if (!accumulate) {
     const long n = (long)B * L.N;
     hipLaunchKernelGGL(k_zero_lut, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, y, n);
   }
-  // about four workgroups per CU over (sub-tiles x K splits x tokens), each
-  // taking 4..16 groups: fewer groups re-copy the tables too often, fewer
-  // workgroups hide too little latency (measured on the Llama3-8B shapes)
+  // groups per workgroup: 4 on layers of up to 4096 (sub-tile, group)
+  // units per token (the Llama3-8B attention projections: 8 and 16 groups
+  // 5% and 30% slower), 16 above (the MLP: 45.2 us against 48.6 with 8 and
+  // 59.1 with 4); fewer groups re-copy the tables too often, more leave too
+  // few workgroups to hide latency
   const long subtiles = (long)L.tiles * (L.T / kSub);
   long splits;
-  int gps = (int)(((long)L.groups * subtiles * B + 1023) / 1024);
-  gps = gps < 4 ? 4 : (gps > 16 ? 16 : gps);
+  int gps = (long)L.groups * subtiles * B <= 4096 ? 4 : 16;
   gps = gps > L.groups ? L.groups : gps;
   if (const char* e = getenv("GRINQH_LUT_GPS")) {
     const int v = atoi(e);
