@@ -81,7 +81,8 @@ WORKLOADS = {
 MFMA_F16_PEAK_TFLOPS = 2500.0
 
 
-PREFILL_SOURCES = ("paper_2606_23419_amd/csrc/prefill.hip", "paper_2606_23419_amd/csrc/grinqh_internal.h")
+PREFILL_SOURCES = ("paper_2606_23419_amd/csrc/prefill.hip", "paper_2606_23419_amd/csrc/grinqh_internal.h",
+                   "paper_2606_23419_amd/csrc/vmm_common.h")
 
 
 def vmm_source_sha() -> str:
