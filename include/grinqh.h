@@ -217,6 +217,16 @@ GRINQH_API int grinqh_vmm_lut(const grinqh_layer_desc* desc, const void* packed_
                               const void* luts, const void* x, const uint8_t* level_map,
                               int32_t B, float* y, int32_t flags, void* stream);
 
+/* The LUT VMM with the threshold assignment of Sec. 3.1 fused into it: each
+ * channel's level is graded inside the kernel from |x| and `thresholds`
+ * (host fp32 theta_1..theta_n, rules as in grinqh_assign), so no level map
+ * is read; if level_map_out is not NULL the levels are also written there
+ * (uint8 [B][K], device).  Other arguments as grinqh_vmm_lut. */
+GRINQH_API int grinqh_vmm_lut_threshold(const grinqh_layer_desc* desc, const void* packed_codes,
+                                        const void* luts, const void* x, int32_t B,
+                                        const float* thresholds, uint8_t* level_map_out, float* y,
+                                        int32_t flags, void* stream);
+
 /* Message of the last failing call on this thread ("" if none). */
 GRINQH_API const char* grinqh_last_error(void);
 

@@ -345,8 +345,28 @@ int grinqh_vmm_lut(const grinqh_layer_desc* desc, const void* packed_codes, cons
   if (((uintptr_t)packed_codes | (uintptr_t)luts) & 15u)
     return fail(GRINQH_EINVAL, "packed codes and luts must be 16-byte aligned");
   if (((uintptr_t)x | (uintptr_t)y) & 3u) return fail(GRINQH_EINVAL, "x and y must be 4-byte aligned");
-  return launch_vmm_lut(L, packed_codes, luts, x, level_map, B, y, flags & GRINQH_VMM_ACCUMULATE,
-                        (hipStream_t)stream);
+  return launch_vmm_lut(L, packed_codes, luts, x, level_map, nullptr, nullptr, B, y,
+                        flags & GRINQH_VMM_ACCUMULATE, (hipStream_t)stream);
+}
+
+int grinqh_vmm_lut_threshold(const grinqh_layer_desc* desc, const void* packed_codes, const void* luts,
+                             const void* x, int32_t B, const float* thresholds, uint8_t* level_map_out,
+                             float* y, int32_t flags, void* stream) {
+  clear_error();
+  Layer L;
+  int st = resolve(desc, &L, nullptr);
+  if (st) return st;
+  if (!packed_codes || !luts || !x || !y) return fail(GRINQH_EINVAL, "codes, luts, x and y must not be NULL");
+  if (B < 1 || B > 65535) return fail(GRINQH_EINVAL, "B=%d outside 1..65535", B);
+  if (flags & ~GRINQH_VMM_ACCUMULATE) return fail(GRINQH_EINVAL, "unknown flags 0x%x", flags);
+  if (((uintptr_t)packed_codes | (uintptr_t)luts) & 15u)
+    return fail(GRINQH_EINVAL, "packed codes and luts must be 16-byte aligned");
+  if (((uintptr_t)x | (uintptr_t)y) & 3u) return fail(GRINQH_EINVAL, "x and y must be 4-byte aligned");
+  Thresholds th;
+  st = check_thresholds(L, thresholds, &th);
+  if (st) return st;
+  return launch_vmm_lut(L, packed_codes, luts, x, nullptr, &th, level_map_out, B, y,
+                        flags & GRINQH_VMM_ACCUMULATE, (hipStream_t)stream);
 }
 
 const char* grinqh_last_error(void) { return g_err; }

@@ -99,7 +99,10 @@ int launch_vmm(const Layer& L, const void* codes, const void* scales, const void
 int launch_prefill(const Layer& L, const void* codes, const void* scales, const void* x, int M,
                    float* y, int accumulate, hipStream_t s);
 int lut_desc(const Layer& L, LutDesc* D);
+// level_map == nullptr with th != nullptr: levels graded from x in the kernel,
+// written to level_map_out if that is not null
 int launch_vmm_lut(const Layer& L, const void* codes, const void* luts, const void* x,
-                   const uint8_t* level_map, int B, float* y, int accumulate, hipStream_t s);
+                   const uint8_t* level_map, const Thresholds* th, uint8_t* level_map_out, int B,
+                   float* y, int accumulate, hipStream_t s);
 
 }  // namespace grinqh

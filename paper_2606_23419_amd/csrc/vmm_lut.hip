@@ -37,7 +37,8 @@ __global__ __launch_bounds__(kLutThreads) void k_vmm_lut(const uint8_t* __restri
                                                         const uint16_t* __restrict__ x,
                                                         const uint8_t* __restrict__ lm,
                                                         float* __restrict__ y, Layer L, LutDesc D,
-                                                        int groups_per_split, int splits) {
+                                                        int groups_per_split, int splits, int fused,
+                                                        Thresholds th, uint8_t* __restrict__ lm_out) {
   constexpr uint32_t MASK = (1u << U) - 1u;
   extern __shared__ __align__(16) uint16_t s_lut[];          // [levels][kSub][2^b]
   __shared__ float s_red[kLutThreads / 64][kSub];
@@ -101,10 +102,28 @@ __global__ __launch_bounds__(kLutThreads) void k_vmm_lut(const uint8_t* __restri
   const int n_top = L.n_levels - 1;
   const int kr0 = g0 * kGroup, nrows = (g1 - g0) * kGroup;   // the workgroup's channels
 
-  // levels and x of the run's channels, staged once (<= kMaxRun channels)
+  // levels and x of the run's channels, staged once (<= kMaxRun channels):
+  // read from the level map, or graded here from |x| against the thresholds
+  // (Sec. 3.1; th.n is 0 without them), the level map then written out once
+  // (by the workgroups of tile 0, sub-tile 0)
   for (int i = tid; i < nrows; i += kLutThreads) {
-    s_lv[i] = (uint8_t)min((int)lm[(size_t)tok * L.K + kr0 + i], n_top);
-    s_x[i] = x[(size_t)tok * L.K + kr0 + i];
+    const size_t k = (size_t)tok * L.K + kr0 + i;
+    const uint16_t xh = x[k];
+    int lv;
+    if (fused) {
+      const float ax = fabsf(h2f(xh));
+      lv = 0;
+#pragma unroll
+      for (int j = 0; j < kMaxLevels - 1; ++j) {
+        if (j >= th.n) break;                // uniform
+        lv += ax >= th.theta[j] ? 1 : 0;
+      }
+      if (lm_out && t == 0 && sub == 0) lm_out[k] = (uint8_t)lv;
+    } else {
+      lv = min((int)lm[k], n_top);
+    }
+    s_lv[i] = (uint8_t)lv;
+    s_x[i] = xh;
   }
   __syncthreads();
 
@@ -213,7 +232,8 @@ int lut_desc(const Layer& L, LutDesc* D) {
 }
 
 int launch_vmm_lut(const Layer& L, const void* codes, const void* luts, const void* x,
-                   const uint8_t* level_map, int B, float* y, int accumulate, hipStream_t s) {
+                   const uint8_t* level_map, const Thresholds* th, uint8_t* level_map_out, int B,
+                   float* y, int accumulate, hipStream_t s) {
   LutDesc D;
   lut_desc(L, &D);
   // <= 64 * 510 * 2 bytes (levels are distinct widths <= 8), plus the quad padding where it fits
@@ -239,12 +259,17 @@ int launch_vmm_lut(const Layer& L, const void* codes, const void* luts, const vo
   gps = gps > kMaxRun / kGroup ? kMaxRun / kGroup : gps;
   splits = (L.groups + gps - 1) / gps;
   const dim3 grid((unsigned)(subtiles * splits), (unsigned)B);
+  Thresholds none{};
+  const Thresholds& tt = th ? *th : none;
+  const int fused = th != nullptr;
   if (L.u == 2)
     hipLaunchKernelGGL(k_vmm_lut<2>, grid, dim3(kLutThreads), lds, s, (const uint8_t*)codes,
-                       (const uint16_t*)luts, (const uint16_t*)x, level_map, y, L, D, gps, (int)splits);
+                       (const uint16_t*)luts, (const uint16_t*)x, level_map, y, L, D, gps, (int)splits,
+                       fused, tt, level_map_out);
   else
     hipLaunchKernelGGL(k_vmm_lut<1>, grid, dim3(kLutThreads), lds, s, (const uint8_t*)codes,
-                       (const uint16_t*)luts, (const uint16_t*)x, level_map, y, L, D, gps, (int)splits);
+                       (const uint16_t*)luts, (const uint16_t*)x, level_map, y, L, D, gps, (int)splits,
+                       fused, tt, level_map_out);
   return check_launch("vmm_lut");
 }
 

@@ -31,7 +31,7 @@ EXPORTED = (
     "grinqh_resolve_desc", "grinqh_packed_bytes", "grinqh_pack", "grinqh_topk_counts",
     "grinqh_workspace_bytes", "grinqh_calibrate", "grinqh_assign", "grinqh_vmm",
     "grinqh_vmm_threshold", "grinqh_prefill", "grinqh_lut_entries", "grinqh_vmm_lut",
-    "grinqh_last_error",
+    "grinqh_vmm_lut_threshold", "grinqh_last_error",
 )
 
 
@@ -79,6 +79,7 @@ def _load():
         "grinqh_prefill": [dp, vp, vp, vp, i32, vp, i32, vp],
         "grinqh_lut_entries": [dp, ctypes.POINTER(sz)],
         "grinqh_vmm_lut": [dp, vp, vp, vp, vp, i32, vp, i32, vp],
+        "grinqh_vmm_lut_threshold": [dp, vp, vp, vp, i32, ctypes.POINTER(ctypes.c_float), vp, vp, i32, vp],
     }
     for name, args in sig.items():
         f = getattr(lib, name)
@@ -344,4 +345,27 @@ def grinqh_vmm_lut(desc: LayerDesc, packed_codes, luts, x, level_map, y=None,
     yp = _dev(y, torch.float32, "y", (B, rd.N))
     flags = GRINQH_VMM_ACCUMULATE if accumulate else 0
     _check(lib.grinqh_vmm_lut(ctypes.byref(rd), cp, lp, xp, mp, B, yp, flags, _stream(stream)))
+    return y
+
+
+def grinqh_vmm_lut_threshold(desc: LayerDesc, packed_codes, luts, x, thresholds, y=None,
+                             level_map_out=None, accumulate: bool = False, stream=None):
+    """The LUT VMM with threshold grading fused in; optionally writes the level map."""
+    torch = _torch()
+    rd = grinqh_resolve_desc(desc)
+    if x.dim() == 1:
+        x = x.view(1, -1)
+    B = int(x.shape[0])
+    cp = _dev(packed_codes, torch.uint8, "packed_codes",
+              (rd.K * rd.N * rd.level_bits[rd.n_levels - 1] // 8,))
+    lp = _dev(luts, torch.float16, "luts", (grinqh_lut_entries(rd),))
+    xp = _dev(x, torch.float16, "x", (B, rd.K))
+    lo = _dev(level_map_out, torch.uint8, "level_map_out", (B, rd.K)) \
+        if level_map_out is not None else None
+    if y is None:
+        y = torch.empty((B, rd.N), dtype=torch.float32, device=x.device)
+    yp = _dev(y, torch.float32, "y", (B, rd.N))
+    flags = GRINQH_VMM_ACCUMULATE if accumulate else 0
+    _check(lib.grinqh_vmm_lut_threshold(ctypes.byref(rd), cp, lp, xp, B, _floats(thresholds), lo, yp,
+                                        flags, _stream(stream)))
     return y

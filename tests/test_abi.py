@@ -209,6 +209,13 @@ def test_lut_entries_and_validation(g):
     assert V(ctypes.byref(d), FAKE, ctypes.c_void_p(0x1008), FAKE, FAKE, 1, FAKE, 0, None) == -1
     assert V(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, 1, FAKE, 8, None) == -1
     assert g.grinqh_last_error()
+    VT = g.lib.grinqh_vmm_lut_threshold
+    assert VT(ctypes.byref(d), FAKE, FAKE, FAKE, 0, _th([1, 2, 3]), None, FAKE, 0, None) == -1
+    assert VT(ctypes.byref(d), FAKE, None, FAKE, 1, _th([1, 2, 3]), None, FAKE, 0, None) == -1
+    assert VT(ctypes.byref(d), FAKE, FAKE, FAKE, 1, None, None, FAKE, 0, None) == -1
+    assert VT(ctypes.byref(d), FAKE, FAKE, FAKE, 1, _th([2, 1, 3]), None, FAKE, 0, None) == -1
+    assert VT(ctypes.byref(d), FAKE, FAKE, FAKE, 1, _th([1, 2, 3]), None, FAKE, 8, None) == -1
+    assert g.grinqh_last_error()
 
 
 def test_binding_rejects_host_tensors(g):

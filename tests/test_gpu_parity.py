@@ -714,6 +714,24 @@ def test_vmm_lut_parity(g, torch, K, N, levels, tile_n):
     assert np.all(L.run(g, torch, x, np.zeros((1, K), dtype=np.uint8)) == 0.0)
 
 
+@pytest.mark.parametrize("K,N,levels,tile_n", LUT_CASES)
+def test_vmm_lut_threshold_fused(g, torch, K, N, levels, tile_n):
+    # grading fused into the LUT VMM: levels bit-exact against the oracle's
+    # threshold assignment (written out once per row), y against the oracle
+    L = LutLayer(g, torch, K, N, levels, layer=K + N + 1, tile_n=tile_n)
+    n = len(levels)
+    for B in (1, 3):
+        x = inputs.activations_t3(K, B, 91, B)
+        ax = np.sort(np.abs(x.astype(np.float32)).ravel())
+        th = ax[np.linspace(0, ax.size - 1, n + 1).astype(int)[1:-1]]
+        lm_out = torch.full((B, K), 255, dtype=torch.uint8, device="cuda")
+        y = g.grinqh_vmm_lut_threshold(L.desc, L.pc, L.luts, _dev(torch, x), th, level_map_out=lm_out)
+        torch.cuda.synchronize()
+        lm = orc.assign_threshold(x, th)
+        assert np.array_equal(_host(lm_out), lm), B
+        assert normwise(_host(y), L.ref(x, lm)) <= TOL, B
+
+
 @pytest.mark.parametrize("levels", [(0, 2, 4, 8), (0, 2, 4, 6)])
 def test_vmm_lut_with_uniform_tables_is_the_uniform_vmm(g, torch, levels):
     # tables holding the uniform reconstruction (one power-of-two scale per
