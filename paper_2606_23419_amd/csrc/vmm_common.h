@@ -73,25 +73,6 @@ __device__ __forceinline__ float phi_minus_offset(int b, int bmax) {
   return (b < bmax ? (float)(1 << (7 - b)) : 0.0f) - 128.0f;
 }
 
-template <int V>
-struct Words {
-  uint32_t w[V];
-};
-
-template <int V>
-__device__ __forceinline__ Words<V> load_words(const uint8_t* p) {
-  Words<V> r;
-  if constexpr (V == 1) {
-    r.w[0] = __builtin_nontemporal_load((const uint32_t*)p);
-  } else {
-    typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-    const u32x2 v = __builtin_nontemporal_load((const u32x2*)p);
-    r.w[0] = v.x;
-    r.w[1] = v.y;
-  }
-  return r;
-}
-
 // Sum of a value over the four 16-lane rows of a wave, in every lane.
 // v_permlane32_swap exchanges the upper 32 lanes of its first operand with
 // the lower 32 of its second, and v_permlane16_swap the odd rows of the first
@@ -176,6 +157,34 @@ __device__ __forceinline__ void assemble_codes(uint32_t w1, uint32_t w2, uint32_
   q[1] = ((O12 & 0x0F0F0F0Fu) << 4) | (O34 & 0x0F0F0F0Fu);
   q[2] = (E12 & 0xF0F0F0F0u) | ((E34 >> 4) & 0x0F0F0F0Fu);
   q[3] = (O12 & 0xF0F0F0F0u) | ((O34 >> 4) & 0x0F0F0F0Fu);
+}
+
+// Buffer loads through a resource that spans one tile's rows (K R bytes from
+// the tile's first row).  An offset at or past kNoRow lies outside every
+// such resource (K <= 2^20 and R <= 2048, so a tile spans at most 2^31
+// bytes), and the hardware returns zero for it without a memory access, so
+// a plane word that must read as zero costs an issue slot and no cache
+// traffic.  A lane's offset within a plane row (below 64 KB) may be added.
+// (The 2-bit list kernels use plain global loads: buffer loads measured 3%
+// slower on their launches of more than one workgroup per CU.)
+constexpr uint32_t kNoRow = 0xFFFF0000u;
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t tile_rsrc(const uint8_t* tile, const Layer& L) {
+  // the base is the same in every lane; taken from the first one so the
+  // compiler keeps the resource in scalar registers (a value it cannot prove
+  // uniform would put each load in a loop over the distinct values)
+  const uint64_t p = (uint64_t)tile;
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)p);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(p >> 32));
+  // word 3: 32-bit data format (a zero format would make every access
+  // return zero), no swizzle, no stride
+  return __builtin_amdgcn_make_buffer_rsrc((void*)(((uint64_t)hi << 32) | lo), (short)0,
+                                           (int)((uint32_t)L.K * (uint32_t)L.RB), 0x00020000);
+}
+
+// One dword of a plane row, streamed (non-temporal).
+__device__ __forceinline__ uint32_t load_plane(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  return __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 2);
 }
 
 }  // namespace vmmdev

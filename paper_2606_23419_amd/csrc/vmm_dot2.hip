@@ -75,6 +75,10 @@ __global__ __launch_bounds__(kThreads) void k_vmm_dot2(
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int t = blockIdx.x % L.tiles;
   const int g0 = (blockIdx.x / L.tiles) * gw;
+  // the row that empty items read (zero coefficients): the workgroup's own
+  // first row, in cache; one row shared by all workgroups of a tile made its
+  // cache lines a hot spot
+  const uint32_t no_row = (uint32_t)(g0 * kGroup) * (uint32_t)L.RB;
   const int ng = min(gw, L.groups - g0);
   const int n_top = L.n_levels - 1;
   const int lg = tid / LPR, li = tid % LPR;
@@ -162,7 +166,7 @@ __global__ __launch_bounds__(kThreads) void k_vmm_dot2(
     }
   }
   for (int i = tid; i < (kThreads / LPR * PB) * DW; i += kThreads)
-    (&s_empty[0][0])[i] = (i % DW == 2) ? ((27u << 10) | (27u << 26)) : 0u;
+    (&s_empty[0][0])[i] = (i % DW == 2) ? ((27u << 10) | (27u << 26)) : (i % DW < 2 ? no_row : 0u);
   __syncthreads();
 
   // pairs at their places; padding and the per-group totals
@@ -218,8 +222,8 @@ __global__ __launch_bounds__(kThreads) void k_vmm_dot2(
         if (slot == 0) {
 #pragma unroll
           for (int w = 3 + NB; w < DW; ++w) d[w] = 0u;
-          if (it == ltot - 1) {   // odd count: the last pair's second slot repeats this one, zero coefficients
-            d[1] = off;
+          if (it == ltot - 1) {   // odd count: the last pair's second slot is empty (zero coefficients)
+            d[1] = no_row;
             reinterpret_cast<uint16_t*>(&d[2])[1] = ex;
 #pragma unroll
             for (int b = 0; b < NB; ++b) reinterpret_cast<uint16_t*>(&d[3 + b])[1] = 0;
@@ -227,15 +231,15 @@ __global__ __launch_bounds__(kThreads) void k_vmm_dot2(
         }
       }
       // pad the list to whole batches with empty descriptors (zero
-      // coefficients, offset 0, a finite exponent word), spread over the
+      // coefficients, a cached row, a finite exponent word), spread over the
       // group's 128 lanes, so the main loop needs no bounds tests; an empty
       // list still gets one batch (its group epilogue runs)
       constexpr int kSlots = kThreads / LPR * PB;
       const int padded = total > 0 ? (total + kSlots - 1) / kSlots * kSlots : kSlots;
       for (int it = total + row; it < padded; it += kGroup) {
         uint32_t* d = s_pairs[gg][it];
-        d[0] = 0u;
-        d[1] = 0u;
+        d[0] = no_row;
+        d[1] = no_row;
         d[2] = (27u << 10) | (27u << 26);
 #pragma unroll
         for (int w = 3; w < DW; ++w) d[w] = 0u;
@@ -256,11 +260,20 @@ __global__ __launch_bounds__(kThreads) void k_vmm_dot2(
   __syncthreads();
 
   // ---- main loop: lane group lg takes pairs lg, lg + 16, ... of every group.
-  // The (group, batch) sequence is walked with two register sets: the loads
-  // of the next batch are in flight while the current one is consumed, across
-  // group boundaries too.  A group with no pairs still gets one (empty) batch
-  // so its epilogue runs and the scale prefetch advances.
-  const uint8_t* tile = codes + (size_t)t * L.K * L.RB + li * 2 * U * V;   // 16 V outputs per lane
+  // The (group, batch) sequence runs through four register sets, three
+  // batches in flight while one is consumed, across group boundaries too.  A
+  // group with no pairs still gets one (empty) batch so its epilogue runs.
+  // 16 V outputs per lane.  With 1-bit planes a lane's fields are two bytes
+  // of a plane row: it loads the aligned dword that holds them (its
+  // neighbour's two bytes are the other half) and keeps its half when the
+  // batch is consumed.  Plane rows start at multiples of four bytes.
+  static_assert(U == 2 || V == 1, "1-bit planes: one 16-output word per lane");
+  const int lane_byte = li * 2 * U * V;
+  // (the base stays the same in every lane and the lane's part is added to
+  // each 32-bit offset, so a load takes a scalar base and one offset register)
+  const uint8_t* tile = codes + (size_t)t * L.K * L.RB;
+  const uint32_t lane_off = (uint32_t)(U == 2 ? lane_byte : (lane_byte & ~3));
+  const int half_sh = U == 2 ? 0 : (lane_byte & 2) * 8;
   float yp[NB][NACC], acc[NB][NACC], off[NB];
 #pragma unroll
   for (int b = 0; b < NB; ++b) {
@@ -294,7 +307,7 @@ __global__ __launch_bounds__(kThreads) void k_vmm_dot2(
   };
   // Issue batch b (b >= nbt reads the all-empty batch).  There is no test
   // and no branch: each group's list is padded to whole batches with empty
-  // descriptors (offset 0, the tile's first row, cached and in bounds; zero
+  // descriptors (the workgroup's first row, cached and in bounds; zero
   // coefficients; a finite exponent word, so masked fields stay finite and
   // cancel).  With straight-line loads the compiler counts them exactly and
   // waits only for the batch being consumed.
@@ -315,23 +328,10 @@ __global__ __launch_bounds__(kThreads) void k_vmm_dot2(
 #pragma unroll
         for (int b = 0; b < NB; ++b) B.xp[q][b] = cw[b];
       }
-      Words<V> u1, u2;
-      if constexpr (U == 2) {
-        u1 = load_words<V>(tile + a.x);
-        u2 = load_words<V>(tile + a.y);
-      } else {
-        // sixteen 1-bit fields moved to bit 2o: the 2-bit field machinery then
-        // reads each as 0 or 1 at the plane's own weight
-#pragma unroll
-        for (int v = 0; v < V; ++v) {
-          u1.w[v] = spread_bits(__builtin_nontemporal_load((const uint16_t*)(tile + a.x) + v));
-          u2.w[v] = spread_bits(__builtin_nontemporal_load((const uint16_t*)(tile + a.y) + v));
-        }
-      }
 #pragma unroll
       for (int v = 0; v < V; ++v) {
-        B.w1[q][v] = u1.w[v];
-        B.w2[q][v] = u2.w[v];
+        B.w1[q][v] = __builtin_nontemporal_load((const uint32_t*)(tile + (a.x + lane_off + 4 * v)));
+        B.w2[q][v] = __builtin_nontemporal_load((const uint32_t*)(tile + (a.y + lane_off + 4 * v)));
       }
     }
   };
@@ -340,9 +340,17 @@ __global__ __launch_bounds__(kThreads) void k_vmm_dot2(
     for (int q = 0; q < PB; ++q) {
 #pragma unroll
       for (int b = 0; b < NB; ++b) off[b] = dot2(B.m4[q], B.xp[q][b], off[b]);
+      if constexpr (U == 2) {
 #pragma unroll
-      for (int v = 0; v < V; ++v)
-        consume_pair<NB, NACC>(B.w1[q][v], B.w2[q][v], B.m4[q], B.xp[q], acc, 16 * v);
+        for (int v = 0; v < V; ++v)
+          consume_pair<NB, NACC>(B.w1[q][v], B.w2[q][v], B.m4[q], B.xp[q], acc, 16 * v);
+      } else {
+        // the lane's sixteen 1-bit fields moved to bit 2o: the 2-bit field
+        // machinery then reads each as 0 or 1 at the plane's own weight
+        const uint32_t w1 = spread_bits((B.w1[q][0] >> half_sh) & 0xFFFFu);
+        const uint32_t w2 = spread_bits((B.w2[q][0] >> half_sh) & 0xFFFFu);
+        consume_pair<NB, NACC>(w1, w2, B.m4[q], B.xp[q], acc, 0);
+      }
     }
   };
   // group epilogue (no global loads): scale from LDS, bias once per output
@@ -374,27 +382,23 @@ __global__ __launch_bounds__(kThreads) void k_vmm_dot2(
     if (b + 1 == bstart[gg + 1]) finish_group(gg);
   };
 
-  // four register sets: batches b+1 .. b+3 are in flight while b is consumed
-  Batch R0, R1, R2, R3;
-  fetch(R0, 0);
-  fetch(R1, 1);
-  fetch(R2, 2);
+  // four register sets: batches b+1 .. b+3 are in flight while b is
+  // consumed.  The inner loop is unrolled so each set is a fixed group of
+  // registers, and its end is a guard rather than an exit: an exit out of the
+  // unrolled body makes the loop header wait for every load in flight.
+  Batch R[4];
+  fetch(R[0], 0);
+  fetch(R[1], 1);
+  fetch(R[2], 2);
   for (int b = 0; b < nbt; b += 4) {
-    fetch(R3, b + 3);
-    consume(R0);
-    after(b);
-    if (b + 1 >= nbt) break;
-    fetch(R0, b + 4);
-    consume(R1);
-    after(b + 1);
-    if (b + 2 >= nbt) break;
-    fetch(R1, b + 5);
-    consume(R2);
-    after(b + 2);
-    if (b + 3 >= nbt) break;
-    fetch(R2, b + 6);
-    consume(R3);
-    after(b + 3);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      fetch(R[(i + 3) % 4], b + i + 3);
+      if (b + i < nbt) {
+        consume(R[i]);
+        after(b + i);
+      }
+    }
   }
 
   // ---- reduce: the four lane groups of a wave with lane swaps, the waves

@@ -133,21 +133,23 @@ __global__ __launch_bounds__(kLutThreads) void k_vmm_lut(const uint8_t* __restri
 
   // Rows rs + 64 m, m = 0, 1, ..., through a ring of four register sets:
   // three rows' plane words are in flight while one row is looked up.  The
-  // loads are unconditional (planes past a row's depth read the tile's first
-  // row, which stays in cache, and are masked to zero when consumed), so the
+  // loads are unconditional (planes past a row's depth, and rows past the
+  // run, load from no row and read zero without a memory access), so the
   // compiler counts them and waits for the row being consumed alone.
   constexpr int kWords = 8 / U;
   constexpr int R = 4;
-  const uint8_t* tile_codes = codes + (size_t)t * L.K * L.RB + col;
+  // 1-bit planes: the lane's two bytes are loaded as the aligned dword that
+  // holds them and its half is kept when the row is consumed (plane rows and
+  // sub-tiles start at multiples of four bytes)
+  const uint32_t lane_off = (uint32_t)(U == 2 ? col : (col & ~3));
+  const int half_sh = U == 2 ? 0 : (col & 2) * 8;
+  const __amdgpu_buffer_rsrc_t rsrc = vmmdev::tile_rsrc(codes + (size_t)t * L.K * L.RB, L);
   auto fetch = [&](int i, uint32_t (&w)[kWords]) __attribute__((always_inline)) {
     const int d = i < nrows ? level_planes(L.planes_packed, s_lv[i]) : 0;
-    const uint8_t* row = tile_codes + (size_t)(kr0 + min(i, nrows - 1)) * L.RB;
+    const uint32_t row = (uint32_t)(kr0 + min(i, nrows - 1)) * (uint32_t)L.RB + lane_off;
 #pragma unroll
-    for (int j = 0; j < kWords; ++j) {
-      const uint8_t* a = j < d ? row + (size_t)j * plane_bytes : tile_codes;
-      if constexpr (U == 2) w[j] = __builtin_nontemporal_load((const uint32_t*)a);
-      else w[j] = __builtin_nontemporal_load((const uint16_t*)a);
-    }
+    for (int j = 0; j < kWords; ++j)
+      w[j] = vmmdev::load_plane(rsrc, j < d ? row + (uint32_t)(j * plane_bytes) : vmmdev::kNoRow);
   };
   auto consume = [&](int i, const uint32_t (&wv)[kWords]) __attribute__((always_inline)) {
     const int lvl = i < nrows ? (int)s_lv[i] : 0;
@@ -155,11 +157,12 @@ __global__ __launch_bounds__(kLutThreads) void k_vmm_lut(const uint8_t* __restri
       const float xv = h2f(s_x[i]);
       const int d = level_planes(L.planes_packed, lvl);
       const int b = d * U;
-      // the 16 outputs' codes left-aligned in 8 bits (planes past d are
-      // zero): byte i of qw[r] is output 4 i + r; q_b is its top b bits
+      // the 16 outputs' codes left-aligned in 8 bits (planes past d were
+      // loaded as zero): byte i of qw[r] is output 4 i + r; q_b is its top
+      // b bits
       uint32_t m[kWords];
 #pragma unroll
-      for (int j = 0; j < kWords; ++j) m[j] = j < d ? wv[j] : 0u;
+      for (int j = 0; j < kWords; ++j) m[j] = U == 2 ? wv[j] : (wv[j] >> half_sh) & 0xFFFFu;
       uint32_t w[4];
       if constexpr (U == 2) {
 #pragma unroll
