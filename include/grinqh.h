@@ -81,7 +81,7 @@ typedef struct {
 
 enum { GRINQH_SRC_FP16_RTN = 0, GRINQH_SRC_CODES_U8 = 1 };
 enum { GRINQH_ASSIGN_THRESHOLD = 0, GRINQH_ASSIGN_TOPK = 1 };
-enum { GRINQH_VMM_ACCUMULATE = 1 };
+enum { GRINQH_VMM_ACCUMULATE = 1, GRINQH_VMM_READAHEAD = 2, GRINQH_VMM_NO_READAHEAD = 4 };
 
 /* Fill the auto fields (plane_bits, tile_n) of *in into *out after
  * validating it.  Host only.  Every other entry point resolves the same way. */
@@ -163,7 +163,14 @@ GRINQH_API int grinqh_assign(const grinqh_layer_desc* desc, int mode, const void
  *   value is read as the top level); y: fp32 [B][N]; 1 <= B <= 4.
  *   flags: 0 -> y is overwritten; GRINQH_VMM_ACCUMULATE -> y += result (the
  *   caller initialised y).  Accumulation order across K is not fixed, so y
- *   is reproducible to rounding, not bit for bit. */
+ *   is reproducible to rounding, not bit for bit.
+ *   Read-ahead hint (B = 1 with 2-bit planes; ignored elsewhere):
+ *   GRINQH_VMM_READAHEAD requests plane 1 of a workgroup's first 128 rows
+ *   before their levels are known, which shortens the launch when few
+ *   channels are skipped and wastes the skipped ones' plane-1 bytes;
+ *   GRINQH_VMM_NO_READAHEAD turns it off; with neither it is on for
+ *   launches of at most 384 workgroups.  Setting both is EINVAL.  The result
+ *   does not depend on it (up to rounding order). */
 GRINQH_API int grinqh_vmm(const grinqh_layer_desc* desc, const void* packed_codes,
                const void* packed_scales, const void* x, const uint8_t* level_map,
                int32_t B, float* y, int32_t flags, void* workspace, size_t ws_bytes,

@@ -254,11 +254,19 @@ int grinqh_assign(const grinqh_layer_desc* desc, int mode, const void* x, int32_
   return fail(GRINQH_EINVAL, "mode=%d is not a known assignment mode", mode);
 }
 
+// the read-ahead hint of the VMM flags: 1 on, 0 off, -1 the launch's own rule
+static int readahead_of(int32_t flags) {
+  return (flags & GRINQH_VMM_READAHEAD) ? 1 : ((flags & GRINQH_VMM_NO_READAHEAD) ? 0 : -1);
+}
+
 static int vmm_common_checks(const Layer& L, const void* codes, const void* scales, const void* x,
                              int32_t B, float* y, int32_t flags) {
   if (!codes || !scales || !x || !y) return fail(GRINQH_EINVAL, "codes, scales, x and y must not be NULL");
   if (B < 1 || B > kMaxB) return fail(GRINQH_EUNSUPPORTED, "B=%d outside 1..%d", B, kMaxB);
-  if (flags & ~GRINQH_VMM_ACCUMULATE) return fail(GRINQH_EINVAL, "unknown flags 0x%x", flags);
+  if (flags & ~(GRINQH_VMM_ACCUMULATE | GRINQH_VMM_READAHEAD | GRINQH_VMM_NO_READAHEAD))
+    return fail(GRINQH_EINVAL, "unknown flags 0x%x", flags);
+  if ((flags & GRINQH_VMM_READAHEAD) && (flags & GRINQH_VMM_NO_READAHEAD))
+    return fail(GRINQH_EINVAL, "GRINQH_VMM_READAHEAD and GRINQH_VMM_NO_READAHEAD together");
   if (((uintptr_t)codes | (uintptr_t)scales) & 15u)
     return fail(GRINQH_EINVAL, "packed codes and scales must be 16-byte aligned");
   if (((uintptr_t)x | (uintptr_t)y) & 3u) return fail(GRINQH_EINVAL, "x and y must be 4-byte aligned");
@@ -279,7 +287,7 @@ int grinqh_vmm(const grinqh_layer_desc* desc, const void* packed_codes, const vo
   if (!level_map) return fail(GRINQH_EINVAL, "level_map is NULL");
   if ((uintptr_t)level_map & 1u) return fail(GRINQH_EINVAL, "level_map must be 2-byte aligned");
   return launch_vmm(L, packed_codes, packed_scales, x, level_map, nullptr, nullptr, B, y,
-                    flags & GRINQH_VMM_ACCUMULATE, (hipStream_t)stream);
+                    flags & GRINQH_VMM_ACCUMULATE, readahead_of(flags), (hipStream_t)stream);
 }
 
 int grinqh_vmm_threshold(const grinqh_layer_desc* desc, const void* packed_codes,
@@ -298,7 +306,7 @@ int grinqh_vmm_threshold(const grinqh_layer_desc* desc, const void* packed_codes
   if (st) return st;
   if ((uintptr_t)level_map_out & 1u) return fail(GRINQH_EINVAL, "level_map_out must be 2-byte aligned");
   return launch_vmm(L, packed_codes, packed_scales, x, nullptr, &th, level_map_out, B, y,
-                    flags & GRINQH_VMM_ACCUMULATE, (hipStream_t)stream);
+                    flags & GRINQH_VMM_ACCUMULATE, readahead_of(flags), (hipStream_t)stream);
 }
 
 int grinqh_prefill(const grinqh_layer_desc* desc, const void* packed_codes,

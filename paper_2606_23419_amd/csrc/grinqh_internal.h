@@ -86,16 +86,17 @@ int launch_assign_topk(const Layer& L, const void* x, int B, const TopkCuts& cut
 int launch_calibrate(const Layer& L, const void* x, int S, const QuantilePos& qp,
                      double* per_sample, float* theta, hipStream_t s);
 bool vmm_pp_supported(const Layer& L, int B);
+// readahead: 1 on, 0 off, -1 on for grids of at most 384 workgroups
 int launch_vmm_pp(const Layer& L, const void* codes, const void* scales, const void* x,
                   const uint8_t* level_map, const Thresholds* th, uint8_t* level_map_out,
-                  float* y, hipStream_t s);
+                  float* y, int readahead, hipStream_t s);
 bool vmm_dot2_supported(const Layer& L);
 int launch_vmm_dot2(const Layer& L, const void* codes, const void* scales, const void* x,
                     const uint8_t* level_map, const Thresholds* th, uint8_t* level_map_out,
                     int B, float* y, hipStream_t s);
 int launch_vmm(const Layer& L, const void* codes, const void* scales, const void* x,
                const uint8_t* level_map, const Thresholds* th, uint8_t* level_map_out,
-               int B, float* y, int accumulate, hipStream_t s);
+               int B, float* y, int accumulate, int readahead, hipStream_t s);
 int launch_prefill(const Layer& L, const void* codes, const void* scales, const void* x, int M,
                    float* y, int accumulate, hipStream_t s);
 int lut_desc(const Layer& L, LutDesc* D);

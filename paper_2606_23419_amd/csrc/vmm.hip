@@ -107,7 +107,7 @@ __global__ __launch_bounds__(kVmmThreads) void k_vmm_v0(
 
 int launch_vmm(const Layer& L, const void* codes, const void* scales, const void* x,
                const uint8_t* level_map, const Thresholds* th, uint8_t* level_map_out,
-               int B, float* y, int accumulate, hipStream_t s) {
+               int B, float* y, int accumulate, int readahead, hipStream_t s) {
   if (!accumulate) {
     const long n = (long)B * L.N;
     hipLaunchKernelGGL(k_zero, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, y, n);
@@ -117,7 +117,7 @@ int launch_vmm(const Layer& L, const void* codes, const void* scales, const void
   const char* force = getenv("GRINQH_VMM_KERNEL");   // "dot2" or "v0": testing and timing only
   const bool want_dot2 = force && force[0] == 'd', want_v0 = force && force[0] == 'v';
   if (!want_dot2 && !want_v0 && vmm_pp_supported(L, B))
-    return launch_vmm_pp(L, codes, scales, x, level_map, th, level_map_out, y, s);
+    return launch_vmm_pp(L, codes, scales, x, level_map, th, level_map_out, y, readahead, s);
   if (!want_v0 && vmm_dot2_supported(L))
     return launch_vmm_dot2(L, codes, scales, x, level_map, th, level_map_out, B, y, s);
   // about 512 workgroups per token over the whole chip

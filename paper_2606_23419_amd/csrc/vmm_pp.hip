@@ -457,13 +457,15 @@ __global__ __launch_bounds__(kThreads) void k_vmm_pp(
 template <int LPR>
 void launch_pp(dim3 grid, hipStream_t s, const void* codes, const void* scales, const void* x,
                const uint8_t* lm, float* y, const Layer& L, int gw, int fused,
-               const Thresholds& th, uint8_t* lm_out) {
+               const Thresholds& th, uint8_t* lm_out, int readahead) {
   // Plane-1 read-ahead pays where a CU holds about one workgroup, whose own
   // prologue is then the only thing to hide the first loads behind; with
   // more workgroups per CU the others hide it, and the read-ahead's level-0
-  // rows only cost bandwidth.  GRINQH_VMM_SPEC=0/1 forces it.
+  // rows only cost bandwidth.  The caller's hint decides when given (it
+  // knows how many channels its budget skips); GRINQH_VMM_SPEC=0/1 forces
+  // it for tests and sweeps.
   const char* forced = getenv("GRINQH_VMM_SPEC");
-  const bool spec = forced ? atoi(forced) != 0 : grid.x <= 384;
+  const bool spec = forced ? atoi(forced) != 0 : (readahead >= 0 ? readahead != 0 : grid.x <= 384);
   if (spec)
     hipLaunchKernelGGL((k_vmm_pp<LPR, 2, GRINQH_PP_DEPTH, 256, true>), grid, dim3(256), 0, s,
                        (const uint8_t*)codes, (const uint16_t*)scales, (const uint16_t*)x, lm, y, L, gw, fused,
@@ -484,7 +486,7 @@ bool vmm_pp_supported(const Layer& L, int B) {
 
 int launch_vmm_pp(const Layer& L, const void* codes, const void* scales, const void* x,
                   const uint8_t* level_map, const Thresholds* th, uint8_t* level_map_out,
-                  float* y, hipStream_t s) {
+                  float* y, int readahead, hipStream_t s) {
   // groups per workgroup: about 512 workgroups, rounded to the nearest
   // count (896 units -> 2, 448 -> 1; measured on the Llama3-8B MLP shapes)
   int gw = (int)(((long)L.tiles * L.groups + 256) / 512);
@@ -497,9 +499,9 @@ int launch_vmm_pp(const Layer& L, const void* codes, const void* scales, const v
   Thresholds none{};
   const Thresholds& tt = th ? *th : none;
   const int fused = th != nullptr;
-  if (L.T == 256) launch_pp<16>(grid, s, codes, scales, x, level_map, y, L, gw, fused, tt, level_map_out);
-  else if (L.T == 512) launch_pp<32>(grid, s, codes, scales, x, level_map, y, L, gw, fused, tt, level_map_out);
-  else launch_pp<64>(grid, s, codes, scales, x, level_map, y, L, gw, fused, tt, level_map_out);
+  if (L.T == 256) launch_pp<16>(grid, s, codes, scales, x, level_map, y, L, gw, fused, tt, level_map_out, readahead);
+  else if (L.T == 512) launch_pp<32>(grid, s, codes, scales, x, level_map, y, L, gw, fused, tt, level_map_out, readahead);
+  else launch_pp<64>(grid, s, codes, scales, x, level_map, y, L, gw, fused, tt, level_map_out, readahead);
   return check_launch("vmm (plane pairs)");
 }
 

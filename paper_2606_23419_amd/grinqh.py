@@ -25,6 +25,8 @@ GRINQH_SRC_CODES_U8 = 1
 GRINQH_ASSIGN_THRESHOLD = 0
 GRINQH_ASSIGN_TOPK = 1
 GRINQH_VMM_ACCUMULATE = 1
+GRINQH_VMM_READAHEAD = 2
+GRINQH_VMM_NO_READAHEAD = 4
 MAX_LEVELS = 9
 
 EXPORTED = (
@@ -243,8 +245,16 @@ def grinqh_assign(desc: LayerDesc, x, mode: int, thresholds=None, counts=None, o
     return out
 
 
+def _vmm_flags(accumulate, readahead):
+    # readahead: None = the library's rule, True / False = the hint flags
+    f = GRINQH_VMM_ACCUMULATE if accumulate else 0
+    if readahead is not None:
+        f |= GRINQH_VMM_READAHEAD if readahead else GRINQH_VMM_NO_READAHEAD
+    return f
+
+
 def grinqh_vmm(desc: LayerDesc, packed_codes, packed_scales, x, level_map, y=None,
-               accumulate: bool = False, stream=None):
+               accumulate: bool = False, stream=None, readahead=None):
     """y fp32 [B, N] = nested-precision VMM of fp16 x [B, K] with level_map [B, K]."""
     torch = _torch()
     rd = grinqh_resolve_desc(desc)
@@ -260,14 +270,15 @@ def grinqh_vmm(desc: LayerDesc, packed_codes, packed_scales, x, level_map, y=Non
     if y is None:
         y = torch.empty((B, rd.N), dtype=torch.float32, device=x.device)
     yp = _dev(y, torch.float32, "y", (B, rd.N))
-    flags = GRINQH_VMM_ACCUMULATE if accumulate else 0
+    flags = _vmm_flags(accumulate, readahead)
     _check(lib.grinqh_vmm(ctypes.byref(rd), cp, sp, xp, lp, B, yp, flags, None, 0,
                           _stream(stream)))
     return y
 
 
 def grinqh_vmm_threshold(desc: LayerDesc, packed_codes, packed_scales, x, thresholds, y=None,
-                         level_map_out=None, accumulate: bool = False, stream=None):
+                         level_map_out=None, accumulate: bool = False, stream=None,
+                         readahead=None):
     """The VMM with threshold grading fused in; optionally writes the level map."""
     torch = _torch()
     rd = grinqh_resolve_desc(desc)
@@ -282,7 +293,7 @@ def grinqh_vmm_threshold(desc: LayerDesc, packed_codes, packed_scales, x, thresh
     if y is None:
         y = torch.empty((B, rd.N), dtype=torch.float32, device=x.device)
     yp = _dev(y, torch.float32, "y", (B, rd.N))
-    flags = GRINQH_VMM_ACCUMULATE if accumulate else 0
+    flags = _vmm_flags(accumulate, readahead)
     _check(lib.grinqh_vmm_threshold(ctypes.byref(rd), cp, sp, xp, B, _floats(thresholds), lo,
                                     yp, flags, None, 0, _stream(stream)))
     return y

@@ -173,11 +173,16 @@ def test_vmm_validation(g):
     assert V(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, 5, FAKE, 0, None, 0, None) == -2
     assert V(ctypes.byref(d), FAKE, FAKE, FAKE, None, 1, FAKE, 0, None, 0, None) == -1
     assert V(ctypes.byref(d), None, FAKE, FAKE, FAKE, 1, FAKE, 0, None, 0, None) == -1
-    assert V(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, 1, FAKE, 4, None, 0, None) == -1
+    assert V(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, 1, FAKE, 8, None, 0, None) == -1   # unknown flag
+    # both read-ahead hints at once
+    both = g.GRINQH_VMM_READAHEAD | g.GRINQH_VMM_NO_READAHEAD
+    assert V(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, 1, FAKE, both, None, 0, None) == -1
+    assert "together" in g.grinqh_last_error()
     VT = g.lib.grinqh_vmm_threshold
     assert VT(ctypes.byref(d), FAKE, FAKE, FAKE, 1, None, None, FAKE, 0, None, 0, None) == -1
     assert VT(ctypes.byref(d), FAKE, FAKE, FAKE, 1, _th([2, 1, 3]), None, FAKE, 0, None, 0, None) == -1
     assert VT(ctypes.byref(d), FAKE, FAKE, FAKE, 9, _th([1, 2, 3]), None, FAKE, 0, None, 0, None) == -2
+    assert VT(ctypes.byref(d), FAKE, FAKE, FAKE, 1, _th([1, 2, 3]), None, FAKE, 6, None, 0, None) == -1
     assert g.grinqh_last_error()
 
 

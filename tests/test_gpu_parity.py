@@ -402,6 +402,31 @@ def test_vmm_plane1_readahead(g, torch, spec, gw, tile_n, levels, monkeypatch):
     assert normwise(_host(yt), orc.vmm_batch(L.codes, L.scales, x, lmt, levels)) <= TOL
 
 
+@pytest.mark.parametrize("readahead", [None, True, False])
+@pytest.mark.parametrize("K,N,tile_n", [(1152, 1024, 512), (4096, 4096, 512), (2048, 8192, 256)])
+def test_vmm_readahead_flags(g, torch, readahead, K, N, tile_n, monkeypatch):
+    # The read-ahead hint passed as VMM flags (no environment override) on a
+    # small grid (auto: on) and a large one (auto: off), through both entry
+    # points, B = 1 (the hint's kernel) and B = 2 (where it is ignored).
+    monkeypatch.delenv("GRINQH_VMM_SPEC", raising=False)
+    levels = (0, 2, 4, 6, 8)
+    L = Layer(g, torch, K, N, levels, cfg=73, tile_n=tile_n)
+    rng = np.random.default_rng(73)
+    for B in (1, 2):
+        lm = rng.integers(0, len(levels), size=(B, K)).astype(np.uint8)
+        x = inputs.activations_t3(K, B, 73, B)
+        y = g.grinqh_vmm(L.desc, L.pc, L.ps, _dev(torch, x), _dev(torch, lm), readahead=readahead)
+        torch.cuda.synchronize()
+        ref = orc.vmm_batch(L.codes, L.scales, x, lm, levels)
+        assert normwise(_host(y), ref) <= TOL, (readahead, K, N, B)
+        ax = np.sort(np.abs(x.astype(np.float32)).ravel())
+        th = ax[np.linspace(0, ax.size - 1, len(levels) + 1).astype(int)[1:-1]]
+        yt = g.grinqh_vmm_threshold(L.desc, L.pc, L.ps, _dev(torch, x), th, readahead=readahead)
+        torch.cuda.synchronize()
+        assert normwise(_host(yt), orc.vmm_batch(L.codes, L.scales, x, orc.assign_threshold(x, th),
+                                                 levels)) <= TOL, (readahead, K, N, B)
+
+
 @pytest.mark.parametrize("gw", ["1", "2", "3", "4"])
 @pytest.mark.parametrize("levels,tile_n", [((0, 2, 4, 6, 8), 256), ((0, 2, 4, 6, 8), 512),
                                            ((0, 2, 4, 6, 8), 1024), ((0, 2, 4, 6), 512),
