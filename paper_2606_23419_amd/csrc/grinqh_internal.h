@@ -37,7 +37,7 @@ __host__ __device__ __forceinline__ int level_planes(uint64_t packed, int level)
 }
 
 struct Thresholds {
-  float theta[kMaxLevels - 1];   // theta_1 .. theta_n
+  float theta[kMaxLevels - 1];   // theta_1 .. theta_n, then +inf (kernels compare all)
   int n;
 };
 

@@ -137,11 +137,9 @@ __global__ __launch_bounds__(kThreads) void k_vmm_dot2(
       int graded = 0;
       const float ax = fabsf(fx);
 #pragma unroll
-      for (int j = 0; j < kMaxLevels - 1; ++j) {
-        if (j >= th.n) break;                // uniform
-        graded += ax >= th.theta[j] ? 1 : 0;
-      }
-      const int lvl = fused ? graded : min((int)(lv[i][b] & 0xFFu), n_top);
+      for (int j = 0; j < kMaxLevels - 1; ++j)   // unused thresholds are +inf: no
+        graded += ax >= th.theta[j] ? 1 : 0;     // branch, all loaded up front
+      const int lvl = min(fused ? graded : (int)(lv[i][b] & 0xFFu), n_top);
       if (fused && lm_out && t == 0 && valid) lm_out[(size_t)b * L.K + (g0 + gg) * kGroup + row] = (uint8_t)lvl;
       const int d = valid ? level_planes(L.planes_packed, lvl) : 0;
       dtok[i][b] = d;

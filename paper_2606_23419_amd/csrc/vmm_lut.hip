@@ -114,10 +114,9 @@ __global__ __launch_bounds__(kLutThreads) void k_vmm_lut(const uint8_t* __restri
       const float ax = fabsf(h2f(xh));
       lv = 0;
 #pragma unroll
-      for (int j = 0; j < kMaxLevels - 1; ++j) {
-        if (j >= th.n) break;                // uniform
-        lv += ax >= th.theta[j] ? 1 : 0;
-      }
+      for (int j = 0; j < kMaxLevels - 1; ++j)   // unused thresholds are +inf: no
+        lv += ax >= th.theta[j] ? 1 : 0;         // branch, all loaded up front
+      lv = min(lv, n_top);
       if (lm_out && t == 0 && sub == 0) lm_out[k] = (uint8_t)lv;
     } else {
       lv = min((int)lm[k], n_top);
