@@ -97,7 +97,6 @@ __global__ __launch_bounds__(kThreads) void k_vmm_pp(
 
   __shared__ __align__(16) uint32_t s_units[kPPMaxGW][kPPMaxUnits][8];
   __shared__ __align__(16) uint32_t s_empty[kSlots][8];   // one all-empty batch
-  __shared__ int s_nbd[kPPMaxGW], s_nb[kPPMaxGW];         // double batches, all batches
   __shared__ float s_beta[kPPMaxGW];
   __shared__ __align__(16) uint16_t s_scale[kPPMaxGW][T];
   __shared__ __align__(16) float s_red[kWaves][T];
@@ -225,11 +224,16 @@ __global__ __launch_bounds__(kThreads) void k_vmm_pp(
   }
   __syncthreads();
 
-  // items at their places; padding and the per-group totals
+  // items at their places; padding and the per-group totals.  Every lane of
+  // a half wave computes its group's batch counts; lanes 0 and 32 hand them
+  // to the whole wave in scalar registers, so the main loop starts without
+  // reading them back from LDS.
+  int nb_g[kPPMaxGW] = {}, nbd_g[kPPMaxGW] = {};   // all batches, double batches
 #pragma unroll
   for (int i = 0; i < kPasses; ++i) {
     if (i > 0 && 2 * i >= ng) break;
     const int gg = 2 * i + half;
+    int nb_v = 0, nbd_v = 0;
     if (gg < ng) {
       int dbase = 0, sbase = 0, dtot = 0, stot = 0;
 #pragma unroll
@@ -285,12 +289,14 @@ __global__ __launch_bounds__(kThreads) void k_vmm_pp(
         reinterpret_cast<uint16_t*>(&U[u * 8 + 4 * sub + 2])[h] = (uint16_t)(27 << 10);
         reinterpret_cast<uint16_t*>(&U[u * 8 + 4 * sub + 3])[h] = 0;
       }
-      if (row == 0) {
-        s_beta[gg] = s_bpart[gg][0] + s_bpart[gg][1] + s_bpart[gg][2] + s_bpart[gg][3];
-        s_nbd[gg] = pad_du / kSlots;
-        s_nb[gg] = (pad_du + pad_su) / kSlots;
-      }
+      if (row == 0) s_beta[gg] = s_bpart[gg][0] + s_bpart[gg][1] + s_bpart[gg][2] + s_bpart[gg][3];
+      nbd_v = pad_du / kSlots;
+      nb_v = (pad_du + pad_su) / kSlots;
     }
+    nb_g[2 * i] = __builtin_amdgcn_readlane(nb_v, 0);
+    nb_g[2 * i + 1] = __builtin_amdgcn_readlane(nb_v, 32);
+    nbd_g[2 * i] = __builtin_amdgcn_readlane(nbd_v, 0);
+    nbd_g[2 * i + 1] = __builtin_amdgcn_readlane(nbd_v, 32);
   }
   // the scales come from HBM and arrive after x: stored last (a quarter of
   // each group's per wave)
@@ -314,8 +320,8 @@ __global__ __launch_bounds__(kThreads) void k_vmm_pp(
   bstart[0] = 0;
 #pragma unroll
   for (int gg = 0; gg < kPPMaxGW; ++gg) {
-    bstart[gg + 1] = bstart[gg] + (gg < ng ? s_nb[gg] : 0);
-    bdbl[gg] = gg < ng ? s_nbd[gg] : 0;
+    bstart[gg + 1] = bstart[gg] + nb_g[gg];
+    bdbl[gg] = nbd_g[gg];
   }
   const int nbt = bstart[kPPMaxGW];
   auto group_of = [&](int b) {
