@@ -63,7 +63,6 @@ __global__ __launch_bounds__(kThreads) void k_vmm_dot2(
 
   __shared__ __align__(16) uint32_t s_pairs[max_gw(NB)][max_pairs(U)][DW];
   __shared__ __align__(16) uint32_t s_empty[kThreads / LPR * PB][DW];   // one all-empty batch
-  __shared__ int s_npairs[max_gw(NB)];
   __shared__ float s_beta[max_gw(NB)][NB];
   __shared__ __align__(16) uint16_t s_scale[max_gw(NB)][T];
   // cross-wave sums, one token at a time (the buffer does not grow with the
@@ -167,11 +166,16 @@ __global__ __launch_bounds__(kThreads) void k_vmm_dot2(
     (&s_empty[0][0])[i] = (i % DW == 2) ? ((27u << 10) | (27u << 26)) : (i % DW < 2 ? no_row : 0u);
   __syncthreads();
 
-  // pairs at their places; padding and the per-group totals
+  // pairs at their places; padding and the per-group totals.  Lanes 0 and
+  // 32 hand each pass's pair counts to the whole wave in scalar registers,
+  // so the main loop starts without reading them back from LDS.
+  static_assert(max_gw(NB) % 2 == 0, "two groups per pass");
+  int np_g[max_gw(NB)] = {};
 #pragma unroll
   for (int i = 0; i < kPasses; ++i) {
     if (i > 0 && 2 * i >= ng) break;
     const int gg = 2 * i + half;
+    int np_v = 0;
     if (gg < ng) {
       int base = 0, ftot = 0, lbase = 0, ltot = 0;
 #pragma unroll
@@ -243,12 +247,14 @@ __global__ __launch_bounds__(kThreads) void k_vmm_dot2(
         for (int w = 3; w < DW; ++w) d[w] = 0u;
       }
       if (row == 0) {
-        s_npairs[gg] = total;
 #pragma unroll
         for (int b = 0; b < NB; ++b)
           s_beta[gg][b] = s_bpart[gg][b][0] + s_bpart[gg][b][1] + s_bpart[gg][b][2] + s_bpart[gg][b][3];
       }
+      np_v = total;
     }
+    np_g[2 * i] = __builtin_amdgcn_readlane(np_v, 0);
+    np_g[2 * i + 1] = __builtin_amdgcn_readlane(np_v, 32);
   }
   // the scales come from HBM and arrive after x: stored last (a quarter of
   // each group's per wave)
@@ -292,7 +298,7 @@ __global__ __launch_bounds__(kThreads) void k_vmm_dot2(
   bstart[0] = 0;
 #pragma unroll
   for (int gg = 0; gg < max_gw(NB); ++gg) {
-    int r = gg < ng ? (s_npairs[gg] + kLaneGroups * PB - 1) / (kLaneGroups * PB) : 0;
+    int r = gg < ng ? (np_g[gg] + kLaneGroups * PB - 1) / (kLaneGroups * PB) : 0;
     if (gg < ng && r == 0) r = 1;   // an empty group still gets its epilogue
     bstart[gg + 1] = bstart[gg] + r;
   }
