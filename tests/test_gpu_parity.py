@@ -423,8 +423,18 @@ def test_vmm_readahead_flags(g, torch, readahead, K, N, tile_n, monkeypatch):
         th = ax[np.linspace(0, ax.size - 1, len(levels) + 1).astype(int)[1:-1]]
         yt = g.grinqh_vmm_threshold(L.desc, L.pc, L.ps, _dev(torch, x), th, readahead=readahead)
         torch.cuda.synchronize()
-        assert normwise(_host(yt), orc.vmm_batch(L.codes, L.scales, x, orc.assign_threshold(x, th),
-                                                 levels)) <= TOL, (readahead, K, N, B)
+        lmt = orc.assign_threshold(x, th)
+        reft = orc.vmm_batch(L.codes, L.scales, x, lmt, levels)
+        assert normwise(_host(yt), reft) <= TOL, (readahead, K, N, B)
+        # the benchmarks' call: accumulate onto a non-zero y, level map written out
+        y0 = rng.standard_normal((B, N)).astype(np.float32)
+        ya = _dev(torch, y0)
+        lo = torch.zeros((B, K), dtype=torch.uint8, device="cuda")
+        g.grinqh_vmm_threshold(L.desc, L.pc, L.ps, _dev(torch, x), th, y=ya, level_map_out=lo,
+                               accumulate=True, readahead=readahead)
+        torch.cuda.synchronize()
+        assert np.array_equal(_host(lo), lmt)
+        assert normwise(_host(ya) - y0, reft) <= TOL, (readahead, K, N, B, "accumulate")
 
 
 @pytest.mark.parametrize("gw", ["1", "2", "3", "4"])
