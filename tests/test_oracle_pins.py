@@ -287,6 +287,56 @@ def test_topk_matches_pairwise_ranks_with_ties():
         assert np.array_equal(np.bincount(got, minlength=4), counts)
 
 
+def test_magnitude_key_orders_every_finite_fp16_like_abs():
+    # App. A.1 ranks channels by |x|.  Every finite fp16 bit pattern (both
+    # signs, +-0, subnormals, +-65504): the key must order them exactly as
+    # |x| in float64 does, with equal keys only for equal magnitudes.
+    bits = np.arange(1 << 16, dtype=np.uint32).astype(np.uint16)
+    x = bits.view(np.float16)
+    x = x[np.isfinite(x)]
+    key = orc.magnitude_key(x)
+    mag = np.abs(x.astype(np.float64))
+    order = np.argsort(mag, kind="stable")
+    k_sorted, m_sorted = key[order], mag[order]
+    assert np.all(np.diff(k_sorted) >= 0)
+    # equal magnitude <=> equal key (e.g. -0.0 and +0.0, x and -x)
+    same_mag = np.diff(m_sorted) == 0
+    same_key = np.diff(k_sorted) == 0
+    assert np.array_equal(same_mag, same_key)
+    assert key[x == np.float16(-65504.0)][0] == key[x == np.float16(65504.0)][0]
+
+
+def test_topk_matches_independent_abs_sort_signed_values():
+    # Independent route to the top-p partition: a stable sort of -|x| in
+    # float64 (ties keep the lower index, reading R7), then levels handed out
+    # from the top in rank order.  Signed inputs with negatives, -0.0,
+    # subnormals and +-65504, so a key that ignored the sign bit wrongly (or
+    # used the signed value) would fail.
+    rng = np.random.default_rng(97)
+    special = np.array([0.0, -0.0, 6e-8, -6e-8, 1e-5, -1e-5, 0.5, -0.5, 2.0, -3.0,
+                        65504.0, -65504.0], dtype=np.float16)
+    for trial in range(60):
+        K = int(rng.integers(1, 300))
+        if trial % 3 == 0:
+            x = rng.choice(special, size=K).astype(np.float16)
+        elif trial % 3 == 1:
+            x = (rng.standard_t(3, K) * 4).astype(np.float16)
+        else:
+            x = np.where(rng.random(K) < 0.5, rng.choice(special, size=K),
+                         rng.standard_normal(K)).astype(np.float16)
+        n_lv = int(rng.integers(2, 6))
+        p = rng.multinomial(10000, [1.0 / n_lv] * n_lv)
+        counts = orc.topk_counts(K, p)
+        got = orc.assign_topk(x, counts)
+        order = np.argsort(-np.abs(x.astype(np.float64)), kind="stable")
+        want = np.empty(K, dtype=np.int64)
+        r = 0
+        for j in range(n_lv - 1, -1, -1):
+            want[order[r:r + counts[j]]] = j
+            r += counts[j]
+        assert got.tolist() == want.tolist(), (trial, x.tolist())
+
+
 def test_topk_exact_budget_on_workload_shapes():
     x = inputs.activations_t3(4096, 2, config=93)
     for p in inputs.BUDGETS[inputs.LEVELS_B].values():
