@@ -85,18 +85,6 @@ PREFILL_SOURCES = ("paper_2606_23419_amd/csrc/prefill.hip", "paper_2606_23419_am
                    "paper_2606_23419_amd/csrc/vmm_common.h")
 
 
-def readahead_hint(levels, p_bp):
-    """The VMM read-ahead hint for a budget (p_bp: level shares in 1/10000).
-    Plane 1 of a workgroup's first rows is read before their levels are
-    known, so the skipped channels' plane-1 bytes are wasted.  Measured on
-    the attention step: with b_max 8 off is 8% faster at 2 bits (30% of the
-    channels skipped) and 1.5% at 3 bits (25%), on is 4% faster at 4 bits
-    (20%); b_max 6 at 3 bits like b_max 8; with b_max 4 at 3 bits on is 5%
-    faster (rows of at most two planes).  Off (False) when more than 20% of
-    the channels are skipped and b_max >= 6, else None (the library's rule)."""
-    return False if levels[-1] >= 6 and p_bp[0] > 2000 else None
-
-
 def vmm_source_sha() -> str:
     return source_sha(VMM_SOURCES)
 
@@ -277,7 +265,6 @@ def run_decode(args, torch, g):
         sys.exit(2)
     budget = args.budget if args.budget is not None else wl["budget"]
     p_bp = inputs.BUDGETS[levels][budget]
-    ra = readahead_hint(levels, p_bp)
     gen = torch.Generator(device=dev)
     gen.manual_seed(5)
     descs = {name: g.grinqh_resolve_desc(g.make_desc(K, N, levels, tile_n=args.tile_n))
@@ -323,12 +310,12 @@ def run_decode(args, torch, g):
                 if mode == "threshold":
                     g.grinqh_vmm_threshold(descs[name], w[name][0], w[name][1], xs[xin], thresholds[xin],
                                            y=out[li][name], level_map_out=lm[xin] if li == 0 else None,
-                                           accumulate=True, readahead=ra)
+                                           accumulate=True)
                 else:
                     g.grinqh_assign(descs[name], xs[xin], g.GRINQH_ASSIGN_TOPK, counts=counts[xin],
                                     out=lm[xin])
                     g.grinqh_vmm(descs[name], w[name][0], w[name][1], xs[xin], lm[xin], y=out[li][name],
-                                 accumulate=True, readahead=ra)
+                                 accumulate=True)
 
     s = torch.cuda.Stream()
     s.wait_stream(torch.cuda.current_stream())
@@ -383,7 +370,6 @@ def run_decode(args, torch, g):
         "config": {"workload": wl_name, "decoder_layers": L, "batch": B, "b_max": bmax,
                    "layers": {n: [K, N] for n, K, N, _, _ in layers}, "levels": list(levels),
                    "budget_bits": budget, "assignment": args.assign, "P_bp": list(p_bp),
-                   "readahead": "off" if ra is False else "auto",
                    "outputs": "one buffer per step, cleared by one fill, VMMs accumulate",
                    "packed_weights_GB": round(packed_gb, 3), "achieved_avg_bits": main["achieved_avg_bits"]},
         "tokens_per_s": round(B / (main["ms_per_step"] * 1e-3), 1),
@@ -680,7 +666,6 @@ def main():
     cfg, levels, layers = wl["cfg"], wl["levels"], wl["layers"]
     budget = args.budget if args.budget is not None else wl["budget"]
     p_bp = inputs.BUDGETS[levels][budget]
-    ra = readahead_hint(levels, p_bp)
     T = args.tokens
     n_inputs = max(xin for *_, xin, _ in layers) + 1
 
@@ -717,11 +702,10 @@ def main():
             out = lm["threshold"][xin][t:t + 1] if first_layer_of_input[xin] == name else None
             g.grinqh_vmm_threshold(descs[name], c[name][0], c[name][1], xs[xin][t:t + 1],
                                    thresholds[xin], y=ybufs[name][t:t + 1], level_map_out=out,
-                                   accumulate=True, readahead=ra)
+                                   accumulate=True)
         else:
             g.grinqh_vmm(descs[name], c[name][0], c[name][1], xs[xin][t:t + 1],
-                         lm["topk"][xin][t:t + 1], y=ybufs[name][t:t + 1], accumulate=True,
-                         readahead=ra)
+                         lm["topk"][xin][t:t + 1], y=ybufs[name][t:t + 1], accumulate=True)
 
     def step(mode, vmm_only=False):
         if not vmm_only:
@@ -820,7 +804,6 @@ def main():
     if main_mode == "threshold" and args.bits_sweep:
         saved = dict(thresholds)
         for bb, pb in inputs.BUDGETS[levels].items():
-            ra = readahead_hint(levels, pb)       # the step's VMM calls read it
             for xin in range(n_inputs):
                 thresholds[xin] = g.grinqh_calibrate(desc_of_input[xin], calib[xin], pb).cpu().numpy()
             with torch.cuda.stream(s):
@@ -837,7 +820,6 @@ def main():
                                 "us_per_vmm": round(us, 3), "GBps": round(gbs, 1),
                                 "frac": round(gbs / HBM_PEAK_GBS, 4)}
         thresholds.update(saved)
-        ra = readahead_hint(levels, p_bp)
 
     # reference shapes (e.g. the unmerged q and k/v projections), same input
     for name, K, N in ([] if args.no_ref else wl["ref"]):
@@ -855,10 +837,10 @@ def main():
                 c = cr[t % Rr]
                 if main_mode == "threshold":
                     g.grinqh_vmm_threshold(d, c[0], c[1], xs[xin][t:t + 1], thresholds[xin],
-                                           y=yr[t:t + 1], accumulate=True, readahead=ra)
+                                           y=yr[t:t + 1], accumulate=True)
                 else:
                     g.grinqh_vmm(d, c[0], c[1], xs[xin][t:t + 1], lm["topk"][xin][t:t + 1],
-                                 y=yr[t:t + 1], accumulate=True, readahead=ra)
+                                 y=yr[t:t + 1], accumulate=True)
         with torch.cuda.stream(s):
             ref_step()
         torch.cuda.synchronize()
@@ -889,8 +871,7 @@ def main():
         "config": {"workload": wl_name, "b_max": int(wl["levels"][-1]),
                    "layers": {n: [K, N] for n, K, N, _, _ in layers},
                    "tokens": T, "batch": 1, "levels": list(levels), "budget_bits": budget,
-                   "assignment": main_mode, "P_bp": list(p_bp), "readahead": "off" if ra is False else "auto",
-                   "weight_copies": R,
+                   "assignment": main_mode, "P_bp": list(p_bp), "weight_copies": R,
                    "calibration_tokens": CALIB_TOKENS if main_mode == "threshold" else None,
                    "achieved_avg_bits": res["avg_bits"]},
         "us_per_vmm": round(us_per_vmm, 3),

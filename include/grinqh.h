@@ -81,14 +81,19 @@ typedef struct {
 
 enum { GRINQH_SRC_FP16_RTN = 0, GRINQH_SRC_CODES_U8 = 1 };
 enum { GRINQH_ASSIGN_THRESHOLD = 0, GRINQH_ASSIGN_TOPK = 1 };
-enum { GRINQH_VMM_ACCUMULATE = 1, GRINQH_VMM_READAHEAD = 2, GRINQH_VMM_NO_READAHEAD = 4 };
+enum { GRINQH_VMM_ACCUMULATE = 1 };
+/* Options of grinqh_set_option, and the kernels GRINQH_OPT_VMM_KERNEL names. */
+enum { GRINQH_OPT_VMM_KERNEL = 1, GRINQH_OPT_GROUPS_PER_WG = 2, GRINQH_OPT_PREFILL_TILE = 3,
+       GRINQH_OPT_LUT_GROUPS = 4 };
+enum { GRINQH_KERNEL_AUTO = 0, GRINQH_KERNEL_PER_PLANE = 1, GRINQH_KERNEL_GENERAL = 2 };
 
-/* Fill the auto fields (plane_bits, tile_n) of *in into *out after
- * validating it.  Host only.  Every other entry point resolves the same way. */
+/* Infrastructure, not an operation of the paper.  Fill the auto fields
+ * (plane_bits, tile_n) of *in into *out after validating it.  Host only.
+ * Every other entry point resolves the same way. */
 GRINQH_API int grinqh_resolve_desc(const grinqh_layer_desc* in, grinqh_layer_desc* out);
 
-/* Sizes of the packed buffers of a layer (host only): codes K*N*b_max/8
- * bytes, scales 2*(K/128)*N bytes. */
+/* Infrastructure, not an operation of the paper: sizes of the packed buffers
+ * of a layer (host only), codes K*N*b_max/8 bytes, scales 2*(K/128)*N bytes. */
 GRINQH_API int grinqh_packed_bytes(const grinqh_layer_desc* desc, size_t* codes_bytes,
                         size_t* scales_bytes);
 
@@ -115,22 +120,24 @@ GRINQH_API int grinqh_pack(const grinqh_layer_desc* desc, int src_kind, const vo
  * >= j; counts_out[j] = C_j - C_{j+1} (n+1 values summing to K).  Host only. */
 GRINQH_API int grinqh_topk_counts(int32_t K, int32_t n_levels, const int32_t* p_bp,
                        int32_t* counts_out);
+/* (p_bp and counts_out each hold exactly n_levels entries.) */
 
-/* Device workspace needed by grinqh_assign / grinqh_vmm for B tokens.  The
- * present kernels need none and report 0; callers may pass NULL/0. */
+/* Infrastructure, not an operation of the paper: device workspace needed by
+ * grinqh_assign / grinqh_vmm for B tokens.  The present kernels need none and
+ * report 0; callers may pass NULL/0. */
 GRINQH_API int grinqh_workspace_bytes(const grinqh_layer_desc* desc, int32_t B, size_t* bytes);
 
 /* Offline threshold calibration (Sec. 3.2 calibration of the thresholds;
  * App. A.1).  x: fp16 [S][K] (device) calibration activations, one sample per
  * row, finite; p_bp: host int32 p_0..p_n in basis points (each >= 0, summing
- * to 10000).  For each sample and each k = 1..n (n = n_levels-1) the sample
- * threshold is the type-7 sample quantile of |x| at q_k = U_k / 10000, U_k =
- * p_0 + .. + p_(k-1): with the K magnitudes sorted ascending a_0 <= .. <=
- * a_(K-1), h = (K-1) U_k / 10000 is split exactly into lo = floor(h) and
- * frac = (h - lo) as a float64 quotient of integers, and the threshold is
- * a_lo + frac * (a_(lo+1) - a_lo) in float64 (a_(lo+1) = a_lo at lo = K-1).
- * theta_k is the float64 mean of the sample thresholds, summed in sample
- * order, rounded to fp32.
+ * to 10000; exactly n_levels entries are read).  For each sample and each
+ * k = 1..n (n = n_levels-1) the sample threshold is the type-7 sample
+ * quantile of |x| at q_k = U_k / 10000, U_k = p_0 + .. + p_(k-1): with the K
+ * magnitudes sorted ascending a_0 <= .. <= a_(K-1), h = (K-1) U_k / 10000 is
+ * split exactly into lo = floor(h) and frac = (h - lo) as a float64 quotient
+ * of integers, and the threshold is a_lo + frac * (a_(lo+1) - a_lo) in
+ * float64 (a_(lo+1) = a_lo at lo = K-1).  theta_k is the float64 mean of the
+ * sample thresholds, summed in sample order, rounded to fp32.
  *   per_sample: device float64 [S][n] scratch, written (8-byte aligned).
  *   theta: device fp32 [n] out.  Requires 1 <= S <= 65535, K <= 16384. */
 GRINQH_API int grinqh_calibrate(const grinqh_layer_desc* desc, const void* x, int32_t S,
@@ -140,13 +147,15 @@ GRINQH_API int grinqh_calibrate(const grinqh_layer_desc* desc, const void* x, in
 /* Per-token precision assignment (Sec. 3.1; App. A.1).
  *   x: fp16 [B][K] (device), finite.
  *   mode GRINQH_ASSIGN_THRESHOLD: thresholds = host fp32 theta_1..theta_n
- *     (n = n_levels-1), non-decreasing, not NaN (+inf allowed); channel k gets
- *     the level l with |x_k| in [theta_l, theta_{l+1}), theta_0 = 0,
- *     theta_{n+1} = +inf, |x| compared in fp32.  counts = NULL.
- *   mode GRINQH_ASSIGN_TOPK: counts = host int32 c_0..c_n summing to K (e.g.
- *     from grinqh_topk_counts).  Channels are ordered by |x| descending, ties
- *     by lower index; the first c_n get level n, the next c_{n-1} level n-1,
- *     and so on.  thresholds = NULL.  Requires K <= 16384.
+ *     (exactly n = n_levels-1 entries are read), non-decreasing, not NaN
+ *     (+inf allowed); channel k gets the level l with |x_k| in
+ *     [theta_l, theta_{l+1}), theta_0 = 0, theta_{n+1} = +inf, |x| compared
+ *     in fp32.  counts = NULL.
+ *   mode GRINQH_ASSIGN_TOPK: counts = host int32 c_0..c_n (exactly n_levels
+ *     entries are read) summing to K (e.g. from grinqh_topk_counts).
+ *     Channels are ordered by |x| descending, ties by lower index; the first
+ *     c_n get level n, the next c_{n-1} level n-1, and so on.
+ *     thresholds = NULL.  Requires K <= 16384.
  *   level_map: uint8 [B][K] (device), the level index per channel. */
 GRINQH_API int grinqh_assign(const grinqh_layer_desc* desc, int mode, const void* x, int32_t B,
                   const float* thresholds, const int32_t* counts, uint8_t* level_map,
@@ -163,14 +172,8 @@ GRINQH_API int grinqh_assign(const grinqh_layer_desc* desc, int mode, const void
  *   value is read as the top level); y: fp32 [B][N]; 1 <= B <= 4.
  *   flags: 0 -> y is overwritten; GRINQH_VMM_ACCUMULATE -> y += result (the
  *   caller initialised y).  Accumulation order across K is not fixed, so y
- *   is reproducible to rounding, not bit for bit.
- *   Read-ahead hint (B = 1 with 2-bit planes; ignored elsewhere):
- *   GRINQH_VMM_READAHEAD requests plane 1 of a workgroup's first 128 rows
- *   before their levels are known, which shortens the launch when few
- *   channels are skipped and wastes the skipped ones' plane-1 bytes;
- *   GRINQH_VMM_NO_READAHEAD turns it off; with neither it is on for
- *   launches of at most 384 workgroups.  Setting both is EINVAL.  The result
- *   does not depend on it (up to rounding order). */
+ *   is reproducible to rounding, not bit for bit.  Any other flag bit is
+ *   GRINQH_EINVAL. */
 GRINQH_API int grinqh_vmm(const grinqh_layer_desc* desc, const void* packed_codes,
                const void* packed_scales, const void* x, const uint8_t* level_map,
                int32_t B, float* y, int32_t flags, void* workspace, size_t ws_bytes,
@@ -202,8 +205,9 @@ GRINQH_API int grinqh_prefill(const grinqh_layer_desc* desc, const void* packed_
                               const void* packed_scales, const void* x, int32_t M, float* y,
                               int32_t flags, void* stream);
 
-/* Number of fp16 table entries of a layer's look-up tables (host only):
- * N * sum over levels l >= 1 of 2^b_l. */
+/* Infrastructure, not an operation of the paper: number of fp16 table
+ * entries of a layer's look-up tables (host only), N * sum over levels
+ * l >= 1 of 2^b_l. */
 GRINQH_API int grinqh_lut_entries(const grinqh_layer_desc* desc, size_t* entries);
 
 /* Decode VMM over non-uniform nested weights read through look-up tables
@@ -234,7 +238,22 @@ GRINQH_API int grinqh_vmm_lut_threshold(const grinqh_layer_desc* desc, const voi
                                         const float* thresholds, uint8_t* level_map_out, float* y,
                                         int32_t flags, void* stream);
 
-/* Message of the last failing call on this thread ("" if none). */
+/* Infrastructure for tests and measurements, not an operation of the paper:
+ * process-wide overrides of launch choices that never change results beyond
+ * rounding order.  Value 0 restores each launcher's own choice.
+ *   GRINQH_OPT_VMM_KERNEL: GRINQH_KERNEL_PER_PLANE or GRINQH_KERNEL_GENERAL
+ *     runs that kernel for B = 1 too (the batch kernels otherwise).
+ *   GRINQH_OPT_GROUPS_PER_WG: 1..4 groups of 128 channels per workgroup
+ *     (kernels that take fewer use their maximum).
+ *   GRINQH_OPT_PREFILL_TILE: 1, 2, 3 = 256x256, 256x128, 128x128 prefill tiles.
+ *   GRINQH_OPT_LUT_GROUPS: 1..16 groups per workgroup of the LUT VMM.
+ * Returns GRINQH_EINVAL for an unknown option or a value out of range.  The
+ * setting is read when a call enqueues its kernels; set it between calls. */
+GRINQH_API int grinqh_set_option(int option, int value);
+
+/* Infrastructure, not an operation of the paper: the message of the last
+ * failing call on this thread ("" if none), valid until that thread's next
+ * call. */
 GRINQH_API const char* grinqh_last_error(void);
 
 #ifdef __cplusplus

@@ -27,6 +27,10 @@ int check_launch(const char* what) {
 
 static void clear_error() { g_err[0] = '\0'; }
 
+static Options g_opt = {};
+
+int option(int Options::*field) { return __atomic_load_n(&(g_opt.*field), __ATOMIC_RELAXED); }
+
 // Validate a descriptor and fill a Layer.
 static int resolve(const grinqh_layer_desc* d, Layer* L, grinqh_layer_desc* out) {
   if (!d) return fail(GRINQH_EINVAL, "desc is NULL");
@@ -254,19 +258,11 @@ int grinqh_assign(const grinqh_layer_desc* desc, int mode, const void* x, int32_
   return fail(GRINQH_EINVAL, "mode=%d is not a known assignment mode", mode);
 }
 
-// the read-ahead hint of the VMM flags: 1 on, 0 off, -1 the launch's own rule
-static int readahead_of(int32_t flags) {
-  return (flags & GRINQH_VMM_READAHEAD) ? 1 : ((flags & GRINQH_VMM_NO_READAHEAD) ? 0 : -1);
-}
-
 static int vmm_common_checks(const Layer& L, const void* codes, const void* scales, const void* x,
                              int32_t B, float* y, int32_t flags) {
   if (!codes || !scales || !x || !y) return fail(GRINQH_EINVAL, "codes, scales, x and y must not be NULL");
   if (B < 1 || B > kMaxB) return fail(GRINQH_EUNSUPPORTED, "B=%d outside 1..%d", B, kMaxB);
-  if (flags & ~(GRINQH_VMM_ACCUMULATE | GRINQH_VMM_READAHEAD | GRINQH_VMM_NO_READAHEAD))
-    return fail(GRINQH_EINVAL, "unknown flags 0x%x", flags);
-  if ((flags & GRINQH_VMM_READAHEAD) && (flags & GRINQH_VMM_NO_READAHEAD))
-    return fail(GRINQH_EINVAL, "GRINQH_VMM_READAHEAD and GRINQH_VMM_NO_READAHEAD together");
+  if (flags & ~GRINQH_VMM_ACCUMULATE) return fail(GRINQH_EINVAL, "unknown flags 0x%x", flags);
   if (((uintptr_t)codes | (uintptr_t)scales) & 15u)
     return fail(GRINQH_EINVAL, "packed codes and scales must be 16-byte aligned");
   if (((uintptr_t)x | (uintptr_t)y) & 3u) return fail(GRINQH_EINVAL, "x and y must be 4-byte aligned");
@@ -287,7 +283,7 @@ int grinqh_vmm(const grinqh_layer_desc* desc, const void* packed_codes, const vo
   if (!level_map) return fail(GRINQH_EINVAL, "level_map is NULL");
   if ((uintptr_t)level_map & 1u) return fail(GRINQH_EINVAL, "level_map must be 2-byte aligned");
   return launch_vmm(L, packed_codes, packed_scales, x, level_map, nullptr, nullptr, B, y,
-                    flags & GRINQH_VMM_ACCUMULATE, readahead_of(flags), (hipStream_t)stream);
+                    flags & GRINQH_VMM_ACCUMULATE, (hipStream_t)stream);
 }
 
 int grinqh_vmm_threshold(const grinqh_layer_desc* desc, const void* packed_codes,
@@ -306,7 +302,7 @@ int grinqh_vmm_threshold(const grinqh_layer_desc* desc, const void* packed_codes
   if (st) return st;
   if ((uintptr_t)level_map_out & 1u) return fail(GRINQH_EINVAL, "level_map_out must be 2-byte aligned");
   return launch_vmm(L, packed_codes, packed_scales, x, nullptr, &th, level_map_out, B, y,
-                    flags & GRINQH_VMM_ACCUMULATE, readahead_of(flags), (hipStream_t)stream);
+                    flags & GRINQH_VMM_ACCUMULATE, (hipStream_t)stream);
 }
 
 int grinqh_prefill(const grinqh_layer_desc* desc, const void* packed_codes,
@@ -375,6 +371,22 @@ int grinqh_vmm_lut_threshold(const grinqh_layer_desc* desc, const void* packed_c
   if (st) return st;
   return launch_vmm_lut(L, packed_codes, luts, x, nullptr, &th, level_map_out, B, y,
                         flags & GRINQH_VMM_ACCUMULATE, (hipStream_t)stream);
+}
+
+int grinqh_set_option(int opt, int value) {
+  clear_error();
+  int Options::*field = nullptr;
+  int lo = 0, hi = 0;
+  switch (opt) {
+    case GRINQH_OPT_VMM_KERNEL: field = &Options::vmm_kernel; hi = GRINQH_KERNEL_GENERAL; break;
+    case GRINQH_OPT_GROUPS_PER_WG: field = &Options::groups_per_wg; hi = 4; break;
+    case GRINQH_OPT_PREFILL_TILE: field = &Options::prefill_tile; hi = 3; break;
+    case GRINQH_OPT_LUT_GROUPS: field = &Options::lut_groups; hi = 16; break;
+    default: return fail(GRINQH_EINVAL, "option=%d is not a known option", opt);
+  }
+  if (value < lo || value > hi) return fail(GRINQH_EINVAL, "option %d: value %d outside %d..%d", opt, value, lo, hi);
+  __atomic_store_n(&(g_opt.*field), value, __ATOMIC_RELAXED);
+  return GRINQH_OK;
 }
 
 const char* grinqh_last_error(void) { return g_err; }

@@ -72,6 +72,16 @@ __device__ __forceinline__ uint16_t f2h_rn(float f) {
   return __builtin_bit_cast(uint16_t, (_Float16)f);
 }
 
+// Launch overrides set through grinqh_set_option (tests and measurements);
+// 0 everywhere means each launcher's own choice.  Read with relaxed loads.
+struct Options {
+  int vmm_kernel;       // GRINQH_KERNEL_*: the batch-1 kernel
+  int groups_per_wg;    // groups of 128 channels per workgroup, where a kernel allows it
+  int prefill_tile;     // 1..3: 256x256, 256x128, 128x128
+  int lut_groups;       // groups per workgroup of the LUT VMM
+};
+int option(int Options::*field);
+
 // Error reporting (per thread), defined in grinqh_api.hip.
 int fail(int status, const char* fmt, ...);
 int check_launch(const char* what);
@@ -86,17 +96,16 @@ int launch_assign_topk(const Layer& L, const void* x, int B, const TopkCuts& cut
 int launch_calibrate(const Layer& L, const void* x, int S, const QuantilePos& qp,
                      double* per_sample, float* theta, hipStream_t s);
 bool vmm_pp_supported(const Layer& L, int B);
-// readahead: 1 on, 0 off, -1 on for grids of at most 384 workgroups
 int launch_vmm_pp(const Layer& L, const void* codes, const void* scales, const void* x,
                   const uint8_t* level_map, const Thresholds* th, uint8_t* level_map_out,
-                  float* y, int readahead, hipStream_t s);
+                  float* y, hipStream_t s);
 bool vmm_dot2_supported(const Layer& L);
 int launch_vmm_dot2(const Layer& L, const void* codes, const void* scales, const void* x,
                     const uint8_t* level_map, const Thresholds* th, uint8_t* level_map_out,
                     int B, float* y, hipStream_t s);
 int launch_vmm(const Layer& L, const void* codes, const void* scales, const void* x,
                const uint8_t* level_map, const Thresholds* th, uint8_t* level_map_out,
-               int B, float* y, int accumulate, int readahead, hipStream_t s);
+               int B, float* y, int accumulate, hipStream_t s);
 int launch_prefill(const Layer& L, const void* codes, const void* scales, const void* x, int M,
                    float* y, int accumulate, hipStream_t s);
 int lut_desc(const Layer& L, LutDesc* D);

@@ -325,16 +325,13 @@ void launch_u(int cfg, const Layer& L, const void* codes, const void* scales, co
 
 // Tile choice: 256 x 256 while that gives at least ~0.6 workgroups per CU
 // (one resident per CU), else 256 x 128 on the same condition, else 128 x 128
-// (short prompts; two resident per CU).  GRINQH_PREFILL_TILE = 0 (256 x 256),
-// 1 (256 x 128) or 2 (128 x 128) forces one.
+// (short prompts; two resident per CU).  GRINQH_OPT_PREFILL_TILE = 1
+// (256 x 256), 2 (256 x 128) or 3 (128 x 128) forces one.
 int launch_prefill(const Layer& L, const void* codes, const void* scales, const void* x, int M,
                    float* y, int accumulate, hipStream_t s) {
   const long mb256 = (M + 255) / 256;
   int cfg = mb256 * (L.N / 256) >= 160 ? 0 : mb256 * (L.N / 128) >= 160 ? 1 : 2;
-  if (const char* e = getenv("GRINQH_PREFILL_TILE")) {
-    const int v = atoi(e);
-    if (v >= 0 && v <= 2) cfg = v;
-  }
+  if (const int v = option(&Options::prefill_tile)) cfg = v - 1;
   if (L.u == 2) launch_u<2>(cfg, L, codes, scales, x, M, y, accumulate, s);
   else launch_u<1>(cfg, L, codes, scales, x, M, y, accumulate, s);
   return check_launch("prefill");

@@ -11,8 +11,6 @@
 //   beta_g = sum_{k in g, level > 0} x_k (phi_b - 128),
 // which is sum_k x_k * s * (t + phi - 128) with the scale factored out.
 // Lane groups are reduced through LDS and added into y with atomics.
-#include <cstdlib>
-
 #include "grinqh_internal.h"
 
 namespace grinqh {
@@ -107,17 +105,17 @@ __global__ __launch_bounds__(kVmmThreads) void k_vmm_v0(
 
 int launch_vmm(const Layer& L, const void* codes, const void* scales, const void* x,
                const uint8_t* level_map, const Thresholds* th, uint8_t* level_map_out,
-               int B, float* y, int accumulate, int readahead, hipStream_t s) {
+               int B, float* y, int accumulate, hipStream_t s) {
   if (!accumulate) {
     const long n = (long)B * L.N;
     hipLaunchKernelGGL(k_zero, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, y, n);
     int st = check_launch("vmm zero-fill");
     if (st) return st;
   }
-  const char* force = getenv("GRINQH_VMM_KERNEL");   // "dot2" or "v0": testing and timing only
-  const bool want_dot2 = force && force[0] == 'd', want_v0 = force && force[0] == 'v';
+  const int force = option(&Options::vmm_kernel);   // tests and measurements
+  const bool want_dot2 = force == GRINQH_KERNEL_PER_PLANE, want_v0 = force == GRINQH_KERNEL_GENERAL;
   if (!want_dot2 && !want_v0 && vmm_pp_supported(L, B))
-    return launch_vmm_pp(L, codes, scales, x, level_map, th, level_map_out, y, readahead, s);
+    return launch_vmm_pp(L, codes, scales, x, level_map, th, level_map_out, y, s);
   if (!want_v0 && vmm_dot2_supported(L))
     return launch_vmm_dot2(L, codes, scales, x, level_map, th, level_map_out, B, y, s);
   // about 512 workgroups per token over the whole chip

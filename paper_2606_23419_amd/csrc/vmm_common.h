@@ -13,6 +13,17 @@ __device__ __forceinline__ float dot2(uint32_t a, uint32_t b, float c) {
                                 false);
 }
 
+// The same dot product in its three-address form (v_dot2_f32_f16): the
+// builtin is emitted as v_dot2c, whose accumulator must also be its
+// destination, and in a loop whose accumulators travel through different
+// registers on different paths the compiler then copies each accumulator
+// before its dot (measured ~130 extra moves in the batch-1 VMM loop).
+__device__ __forceinline__ float dot2r(uint32_t a, uint32_t b, float c) {
+  float d;
+  asm("v_dot2_f32_f16 %0, %1, %2, %3" : "=v"(d) : "v"(a), "v"(b), "v"(c));
+  return d;
+}
+
 // Number of set predicates in lanes below this one, and in the whole wave.
 __device__ __forceinline__ int lanes_below(bool pred) {
   const uint64_t m = __ballot(pred);

@@ -25,7 +25,6 @@
 //   off_g  = sum over the group's pairs of 64 (x_k1 w_1 + x_k2 w_2),
 //   beta_g = sum_{k: level > 0} x_k (phi_b - 128)  (midpoint bias, offset),
 // which equals sum_k x_k s (t_k + phi - 128) with t_k the truncated code.
-#include <cstdlib>
 #include <type_traits>
 
 #include "grinqh_internal.h"
@@ -449,11 +448,7 @@ bool vmm_dot2_supported(const Layer& L) {
 }
 
 int vmm_dot2_groups_per_wg(const Layer& L) {
-  const char* env = getenv("GRINQH_VMM_GW");
-  if (env) {
-    const int v = atoi(env);
-    if (v >= 1 && v <= kMaxGW) return v;
-  }
+  if (const int v = option(&Options::groups_per_wg)) return v <= kMaxGW ? v : kMaxGW;
   // 2-bit planes: about 512 workgroups (two per CU), rounded to the nearest
   // count (decode B = 2, 4 at 896 units: -4 to -10% with 2 groups).  1-bit
   // planes: one group per workgroup below 1536 units (Qwen3-8B at T = 512:

@@ -254,10 +254,7 @@ int launch_vmm_lut(const Layer& L, const void* codes, const void* luts, const vo
   long splits;
   int gps = (long)L.groups * subtiles * B <= 4096 ? 4 : 16;
   gps = gps > L.groups ? L.groups : gps;
-  if (const char* e = getenv("GRINQH_LUT_GPS")) {
-    const int v = atoi(e);
-    if (v >= 1 && v <= L.groups) gps = v;
-  }
+  if (const int v = option(&Options::lut_groups)) gps = v <= L.groups ? v : L.groups;
   gps = gps > kMaxRun / kGroup ? kMaxRun / kGroup : gps;
   splits = (L.groups + gps - 1) / gps;
   const dim3 grid((unsigned)(subtiles * splits), (unsigned)B);

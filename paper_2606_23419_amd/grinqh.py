@@ -25,15 +25,20 @@ GRINQH_SRC_CODES_U8 = 1
 GRINQH_ASSIGN_THRESHOLD = 0
 GRINQH_ASSIGN_TOPK = 1
 GRINQH_VMM_ACCUMULATE = 1
-GRINQH_VMM_READAHEAD = 2
-GRINQH_VMM_NO_READAHEAD = 4
+GRINQH_OPT_VMM_KERNEL = 1
+GRINQH_OPT_GROUPS_PER_WG = 2
+GRINQH_OPT_PREFILL_TILE = 3
+GRINQH_OPT_LUT_GROUPS = 4
+GRINQH_KERNEL_AUTO = 0
+GRINQH_KERNEL_PER_PLANE = 1
+GRINQH_KERNEL_GENERAL = 2
 MAX_LEVELS = 9
 
 EXPORTED = (
     "grinqh_resolve_desc", "grinqh_packed_bytes", "grinqh_pack", "grinqh_topk_counts",
     "grinqh_workspace_bytes", "grinqh_calibrate", "grinqh_assign", "grinqh_vmm",
     "grinqh_vmm_threshold", "grinqh_prefill", "grinqh_lut_entries", "grinqh_vmm_lut",
-    "grinqh_vmm_lut_threshold", "grinqh_last_error",
+    "grinqh_vmm_lut_threshold", "grinqh_set_option", "grinqh_last_error",
 )
 
 
@@ -82,6 +87,7 @@ def _load():
         "grinqh_lut_entries": [dp, ctypes.POINTER(sz)],
         "grinqh_vmm_lut": [dp, vp, vp, vp, vp, i32, vp, i32, vp],
         "grinqh_vmm_lut_threshold": [dp, vp, vp, vp, i32, ctypes.POINTER(ctypes.c_float), vp, vp, i32, vp],
+        "grinqh_set_option": [ctypes.c_int, ctypes.c_int],
     }
     for name, args in sig.items():
         f = getattr(lib, name)
@@ -116,6 +122,19 @@ def grinqh_last_error() -> str:
     return lib.grinqh_last_error().decode()
 
 
+def grinqh_set_option(option: int, value: int) -> None:
+    """Process-wide launch override for tests and measurements (see grinqh.h)."""
+    _check(lib.grinqh_set_option(int(option), int(value)))
+
+
+def _host_array(vals, n, ctype, name):
+    """A ctypes array of exactly n host values: the C side reads n entries."""
+    vals = list(vals)
+    if len(vals) != n:
+        raise ValueError(f"{name} has {len(vals)} entries, expected {n}")
+    return (ctype * n)(*vals)
+
+
 def grinqh_resolve_desc(desc: LayerDesc) -> LayerDesc:
     out = LayerDesc()
     _check(lib.grinqh_resolve_desc(ctypes.byref(desc), ctypes.byref(out)))
@@ -130,7 +149,7 @@ def grinqh_packed_bytes(desc: LayerDesc):
 
 def grinqh_topk_counts(K: int, p_bp):
     n = len(p_bp)
-    arr = (ctypes.c_int32 * n)(*[int(v) for v in p_bp])
+    arr = _host_array([int(v) for v in p_bp], n, ctypes.c_int32, "p_bp")
     out = (ctypes.c_int32 * n)()
     _check(lib.grinqh_topk_counts(int(K), n, arr, out))
     return [int(v) for v in out]
@@ -200,9 +219,8 @@ def grinqh_pack(desc: LayerDesc, W=None, codes=None, scales=None, out_codes=None
     return out_codes, out_scales
 
 
-def _floats(vals):
-    vals = [float(v) for v in vals]
-    return (ctypes.c_float * max(1, len(vals)))(*vals)
+def _thresholds(rd, vals):
+    return _host_array([float(v) for v in vals], rd.n_levels - 1, ctypes.c_float, "thresholds")
 
 
 def grinqh_calibrate(desc: LayerDesc, x, p_bp, per_sample=None, theta=None, stream=None):
@@ -221,7 +239,7 @@ def grinqh_calibrate(desc: LayerDesc, x, p_bp, per_sample=None, theta=None, stre
         theta = torch.empty((n,), dtype=torch.float32, device=x.device)
     pp = _dev(per_sample, torch.float64, "per_sample", (S, n))
     tp = _dev(theta, torch.float32, "theta", (n,))
-    arr = (ctypes.c_int32 * len(p_bp))(*[int(v) for v in p_bp])
+    arr = _host_array([int(v) for v in p_bp], rd.n_levels, ctypes.c_int32, "p_bp")
     _check(lib.grinqh_calibrate(ctypes.byref(rd), xp, S, arr, pp, tp, _stream(stream)))
     return theta
 
@@ -238,23 +256,20 @@ def grinqh_assign(desc: LayerDesc, x, mode: int, thresholds=None, counts=None, o
     if out is None:
         out = torch.empty((B, rd.K), dtype=torch.uint8, device=x.device)
     op = _dev(out, torch.uint8, "out", (B, rd.K))
-    th = _floats(thresholds) if thresholds is not None else None
-    cn = (ctypes.c_int32 * len(counts))(*[int(c) for c in counts]) if counts is not None else None
+    th = _thresholds(rd, thresholds) if thresholds is not None else None
+    cn = _host_array([int(c) for c in counts], rd.n_levels, ctypes.c_int32, "counts") \
+        if counts is not None else None
     _check(lib.grinqh_assign(ctypes.byref(rd), int(mode), xp, B, th, cn, op, None, 0,
                              _stream(stream)))
     return out
 
 
-def _vmm_flags(accumulate, readahead):
-    # readahead: None = the library's rule, True / False = the hint flags
-    f = GRINQH_VMM_ACCUMULATE if accumulate else 0
-    if readahead is not None:
-        f |= GRINQH_VMM_READAHEAD if readahead else GRINQH_VMM_NO_READAHEAD
-    return f
+def _vmm_flags(accumulate):
+    return GRINQH_VMM_ACCUMULATE if accumulate else 0
 
 
 def grinqh_vmm(desc: LayerDesc, packed_codes, packed_scales, x, level_map, y=None,
-               accumulate: bool = False, stream=None, readahead=None):
+               accumulate: bool = False, stream=None):
     """y fp32 [B, N] = nested-precision VMM of fp16 x [B, K] with level_map [B, K]."""
     torch = _torch()
     rd = grinqh_resolve_desc(desc)
@@ -270,15 +285,14 @@ def grinqh_vmm(desc: LayerDesc, packed_codes, packed_scales, x, level_map, y=Non
     if y is None:
         y = torch.empty((B, rd.N), dtype=torch.float32, device=x.device)
     yp = _dev(y, torch.float32, "y", (B, rd.N))
-    flags = _vmm_flags(accumulate, readahead)
+    flags = _vmm_flags(accumulate)
     _check(lib.grinqh_vmm(ctypes.byref(rd), cp, sp, xp, lp, B, yp, flags, None, 0,
                           _stream(stream)))
     return y
 
 
 def grinqh_vmm_threshold(desc: LayerDesc, packed_codes, packed_scales, x, thresholds, y=None,
-                         level_map_out=None, accumulate: bool = False, stream=None,
-                         readahead=None):
+                         level_map_out=None, accumulate: bool = False, stream=None):
     """The VMM with threshold grading fused in; optionally writes the level map."""
     torch = _torch()
     rd = grinqh_resolve_desc(desc)
@@ -293,8 +307,8 @@ def grinqh_vmm_threshold(desc: LayerDesc, packed_codes, packed_scales, x, thresh
     if y is None:
         y = torch.empty((B, rd.N), dtype=torch.float32, device=x.device)
     yp = _dev(y, torch.float32, "y", (B, rd.N))
-    flags = _vmm_flags(accumulate, readahead)
-    _check(lib.grinqh_vmm_threshold(ctypes.byref(rd), cp, sp, xp, B, _floats(thresholds), lo,
+    flags = _vmm_flags(accumulate)
+    _check(lib.grinqh_vmm_threshold(ctypes.byref(rd), cp, sp, xp, B, _thresholds(rd, thresholds), lo,
                                     yp, flags, None, 0, _stream(stream)))
     return y
 
@@ -377,6 +391,6 @@ def grinqh_vmm_lut_threshold(desc: LayerDesc, packed_codes, luts, x, thresholds,
         y = torch.empty((B, rd.N), dtype=torch.float32, device=x.device)
     yp = _dev(y, torch.float32, "y", (B, rd.N))
     flags = GRINQH_VMM_ACCUMULATE if accumulate else 0
-    _check(lib.grinqh_vmm_lut_threshold(ctypes.byref(rd), cp, lp, xp, B, _floats(thresholds), lo, yp,
+    _check(lib.grinqh_vmm_lut_threshold(ctypes.byref(rd), cp, lp, xp, B, _thresholds(rd, thresholds), lo, yp,
                                         flags, _stream(stream)))
     return y

@@ -1,5 +1,5 @@
 """Host-side logic of bench.py: the algorithmic byte counts behind the
-reported GB/s, the read-ahead policy and the one-GPU guard (no GPU needed)."""
+reported GB/s and the one-GPU guard (no GPU needed)."""
 import subprocess
 import sys
 import os
@@ -41,14 +41,6 @@ def test_bytes_required_batch_reads_union_depth_once():
     # one token alone is the batch-1 count
     assert bench.bytes_required_batch(a[:1], (0, 2, 4, 8), K, N, False) == \
         int(bench.bytes_required(a[:1], (0, 2, 4, 8), K, N, False)[0])
-
-
-@pytest.mark.parametrize("levels", list(inputs.BUDGETS))
-def test_readahead_hint_policy(levels):
-    # off exactly where more than 20% of the channels are skipped at b_max >= 6
-    for budget, p in inputs.BUDGETS[levels].items():
-        want = False if (levels[-1] >= 6 and p[0] > 2000) else None
-        assert bench.readahead_hint(levels, p) is want, (levels, budget)
 
 
 def test_bench_refuses_several_gpus():

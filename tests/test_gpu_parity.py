@@ -27,6 +27,22 @@ def torch():
     return t
 
 
+@pytest.fixture
+def opts(g):
+    """Set launch overrides (grinqh_set_option) for one test, reset after it."""
+    touched = []
+
+    def setopt(option, value):
+        g.grinqh_set_option(option, int(value))
+        touched.append(option)
+    yield setopt
+    for option in touched:
+        g.grinqh_set_option(option, 0)
+
+
+KERNEL = {"dot2": 1, "v0": 2}   # GRINQH_KERNEL_PER_PLANE, GRINQH_KERNEL_GENERAL
+
+
 def _dev(torch, a):
     return torch.from_numpy(np.ascontiguousarray(a)).cuda()
 
@@ -352,12 +368,12 @@ def test_full_size_pack_and_sampled_vmm(g, torch, name, K, N, levels, xkind):
 @pytest.mark.parametrize("kernel", ["pp", "dot2"])
 @pytest.mark.parametrize("gw", ["1", "2", "3", "4"])
 @pytest.mark.parametrize("tile_n", [256, 512, 1024])
-def test_vmm_groups_per_workgroup(g, torch, gw, tile_n, kernel, monkeypatch):
+def test_vmm_groups_per_workgroup(g, torch, gw, tile_n, kernel, opts):
     # K = 1152 is 9 groups: every gw > 1 leaves a ragged last workgroup.  At
     # B = 1 the plane-pair kernel runs unless the per-plane kernel is forced.
-    monkeypatch.setenv("GRINQH_VMM_GW", gw)
+    opts(g.GRINQH_OPT_GROUPS_PER_WG, gw)
     if kernel == "dot2":
-        monkeypatch.setenv("GRINQH_VMM_KERNEL", "dot2")
+        opts(g.GRINQH_OPT_VMM_KERNEL, g.GRINQH_KERNEL_PER_PLANE)
     levels = (0, 2, 4, 6, 8)
     K, N = 1152, 1024
     L = Layer(g, torch, K, N, levels, cfg=64, tile_n=tile_n)
@@ -369,18 +385,16 @@ def test_vmm_groups_per_workgroup(g, torch, gw, tile_n, kernel, monkeypatch):
         assert normwise(y, ref) <= TOL, (gw, tile_n, B, normwise(y, ref))
 
 
-@pytest.mark.parametrize("spec", ["0", "1"])
-@pytest.mark.parametrize("gw", ["1", "2", "3", "4"])
+@pytest.mark.parametrize("gw", ["1", "2"])
 @pytest.mark.parametrize("tile_n", [256, 512, 1024])
 @pytest.mark.parametrize("levels", [(0, 2, 4, 6, 8), (0, 2, 4, 6), (0, 2, 4)])
-def test_vmm_plane1_readahead(g, torch, spec, gw, tile_n, levels, monkeypatch):
-    # The batch-1 plane-pair kernel with the plane-1 read-ahead forced on or
-    # off, for every groups-per-workgroup count (only the first group of a
-    # workgroup is read ahead), b_max 8, 6 and 4, through the level-map and
-    # the fused-threshold entry points.  K = 1152 is 9 groups: ragged last
-    # workgroups for gw > 1.
-    monkeypatch.setenv("GRINQH_VMM_SPEC", spec)
-    monkeypatch.setenv("GRINQH_VMM_GW", gw)
+def test_vmm_batch1_depth_classes(g, torch, gw, tile_n, levels, opts):
+    # The batch-1 kernel sorts each wave's rows into those read to 3-4 planes
+    # and those read to 1-2, and pads each class to whole batches: a group
+    # with nothing to read, one at full depth, and random depths, for b_max
+    # 8, 6 and 4, through the level-map and the fused-threshold entry points.
+    # K = 1152 is 9 groups: a ragged last workgroup at gw = 2.
+    opts(g.GRINQH_OPT_GROUPS_PER_WG, gw)
     K, N = 1152, 1024
     L = Layer(g, torch, K, N, levels, cfg=69, tile_n=tile_n)
     rng = np.random.default_rng(69)
@@ -388,9 +402,10 @@ def test_vmm_plane1_readahead(g, torch, spec, gw, tile_n, levels, monkeypatch):
     lm = rng.integers(0, n, size=(1, K)).astype(np.uint8)
     lm[0, :128] = 0                            # a first group with nothing to read
     lm[0, 256:384] = n - 1                     # and one at full depth
-    x = inputs.activations_t3(K, 1, 69, int(spec) * 16 + int(gw))
+    lm[0, 512:544] = 1                         # a wave slice with only shallow rows
+    x = inputs.activations_t3(K, 1, 69, int(gw))
     y, ref = _vmm_case(g, torch, L, x, lm)
-    assert normwise(y, ref) <= TOL, (spec, gw, tile_n, levels, normwise(y, ref))
+    assert normwise(y, ref) <= TOL, (gw, tile_n, levels, normwise(y, ref))
     # fused grading: thresholds at quantiles of |x|, level map written out
     ax = np.sort(np.abs(x[0].astype(np.float32)))
     th = ax[np.linspace(0, K - 1, n + 1).astype(int)[1:-1]]
@@ -402,52 +417,50 @@ def test_vmm_plane1_readahead(g, torch, spec, gw, tile_n, levels, monkeypatch):
     assert normwise(_host(yt), orc.vmm_batch(L.codes, L.scales, x, lmt, levels)) <= TOL
 
 
-@pytest.mark.parametrize("readahead", [None, True, False])
 @pytest.mark.parametrize("K,N,tile_n", [(1152, 1024, 512), (4096, 4096, 512), (2048, 8192, 256)])
-def test_vmm_readahead_flags(g, torch, readahead, K, N, tile_n, monkeypatch):
-    # The read-ahead hint passed as VMM flags (no environment override) on a
-    # small grid (auto: on) and a large one (auto: off), through both entry
-    # points, B = 1 (the hint's kernel) and B = 2 (where it is ignored).
-    monkeypatch.delenv("GRINQH_VMM_SPEC", raising=False)
+def test_vmm_entry_points_and_accumulate(g, torch, K, N, tile_n):
+    # Both entry points on a small grid and a large one, B = 1 and B = 2,
+    # and the benchmarks' call: accumulate onto a non-zero y with the level
+    # map written out.
     levels = (0, 2, 4, 6, 8)
     L = Layer(g, torch, K, N, levels, cfg=73, tile_n=tile_n)
     rng = np.random.default_rng(73)
     for B in (1, 2):
         lm = rng.integers(0, len(levels), size=(B, K)).astype(np.uint8)
         x = inputs.activations_t3(K, B, 73, B)
-        y = g.grinqh_vmm(L.desc, L.pc, L.ps, _dev(torch, x), _dev(torch, lm), readahead=readahead)
+        y = g.grinqh_vmm(L.desc, L.pc, L.ps, _dev(torch, x), _dev(torch, lm), )
         torch.cuda.synchronize()
         ref = orc.vmm_batch(L.codes, L.scales, x, lm, levels)
-        assert normwise(_host(y), ref) <= TOL, (readahead, K, N, B)
+        assert normwise(_host(y), ref) <= TOL, (K, N, B)
         ax = np.sort(np.abs(x.astype(np.float32)).ravel())
         th = ax[np.linspace(0, ax.size - 1, len(levels) + 1).astype(int)[1:-1]]
-        yt = g.grinqh_vmm_threshold(L.desc, L.pc, L.ps, _dev(torch, x), th, readahead=readahead)
+        yt = g.grinqh_vmm_threshold(L.desc, L.pc, L.ps, _dev(torch, x), th, )
         torch.cuda.synchronize()
         lmt = orc.assign_threshold(x, th)
         reft = orc.vmm_batch(L.codes, L.scales, x, lmt, levels)
-        assert normwise(_host(yt), reft) <= TOL, (readahead, K, N, B)
+        assert normwise(_host(yt), reft) <= TOL, (K, N, B)
         # the benchmarks' call: accumulate onto a non-zero y, level map written out
         y0 = rng.standard_normal((B, N)).astype(np.float32)
         ya = _dev(torch, y0)
         lo = torch.zeros((B, K), dtype=torch.uint8, device="cuda")
         g.grinqh_vmm_threshold(L.desc, L.pc, L.ps, _dev(torch, x), th, y=ya, level_map_out=lo,
-                               accumulate=True, readahead=readahead)
+                               accumulate=True, )
         torch.cuda.synchronize()
         assert np.array_equal(_host(lo), lmt)
-        assert normwise(_host(ya) - y0, reft) <= TOL, (readahead, K, N, B, "accumulate")
+        assert normwise(_host(ya) - y0, reft) <= TOL, (K, N, B, "accumulate")
 
 
 @pytest.mark.parametrize("gw", ["1", "2", "3", "4"])
 @pytest.mark.parametrize("levels,tile_n", [((0, 2, 4, 6, 8), 256), ((0, 2, 4, 6, 8), 512),
                                            ((0, 2, 4, 6, 8), 1024), ((0, 2, 4, 6), 512),
                                            ((0, 2, 3, 4, 8), 512), ((0, 2, 3, 4, 8), 1024)])
-def test_vmm_per_plane_depth_mix(g, torch, gw, levels, tile_n, monkeypatch):
+def test_vmm_per_plane_depth_mix(g, torch, gw, levels, tile_n, opts):
     # The per-plane kernel (batches, 1-bit planes, and 2-bit planes at B = 1
     # when forced): per-token depths, lone last planes paired across rows
     # (odd and even counts of them), ragged workgroups (K = 1152), through
     # the level-map and the fused-threshold entry points.
-    monkeypatch.setenv("GRINQH_VMM_GW", gw)
-    monkeypatch.setenv("GRINQH_VMM_KERNEL", "dot2")
+    opts(g.GRINQH_OPT_GROUPS_PER_WG, gw)
+    opts(g.GRINQH_OPT_VMM_KERNEL, g.GRINQH_KERNEL_PER_PLANE)
     K, N = 1152, 1024
     L = Layer(g, torch, K, N, levels, cfg=71, tile_n=tile_n)
     rng = np.random.default_rng(71)
@@ -470,10 +483,10 @@ def test_vmm_per_plane_depth_mix(g, torch, gw, levels, tile_n, monkeypatch):
 
 
 @pytest.mark.parametrize("kernel", ["pp", "dot2"])
-def test_vmm_precision_margin(g, torch, kernel, monkeypatch):
+def test_vmm_precision_margin(g, torch, kernel, opts):
     # the contract is 1e-3; the fp32 accumulation should sit far below it
     if kernel == "dot2":
-        monkeypatch.setenv("GRINQH_VMM_KERNEL", "dot2")
+        opts(g.GRINQH_OPT_VMM_KERNEL, g.GRINQH_KERNEL_PER_PLANE)
     levels = (0, 2, 4, 6, 8)
     K, N = 4096, 1024
     L = Layer(g, torch, K, N, levels, cfg=65, tile_n=256)
@@ -490,11 +503,11 @@ def test_vmm_precision_margin(g, torch, kernel, monkeypatch):
 
 @pytest.mark.parametrize("tile_n", [256, 512, 1024])
 @pytest.mark.parametrize("gw", ["1", "2", "4"])
-def test_vmm_groups_with_no_active_channel(g, torch, tile_n, gw, monkeypatch):
+def test_vmm_groups_with_no_active_channel(g, torch, tile_n, gw, opts):
     # groups whose channels are all skipped, next to active ones in the same
     # workgroup: such a group has no plane rows to read but still runs its
     # epilogue (regression: its padding once left the batch unwritten)
-    monkeypatch.setenv("GRINQH_VMM_GW", gw)
+    opts(g.GRINQH_OPT_GROUPS_PER_WG, gw)
     levels = (0, 2, 4, 6, 8)
     K, N = 1024, 1024
     L = Layer(g, torch, K, N, levels, cfg=66, tile_n=tile_n)
@@ -623,8 +636,8 @@ def test_prefill_full_size_sampled(g, torch, name, K, N, levels, M):
     (640, 1024, (0, 2, 3, 4, 8), 512, 257),    # 1-bit planes
     (256, 2048, (0, 2, 4, 6, 8), 2048, 64),
 ])
-def test_prefill_tile_configs(g, torch, tile, K, N, levels, tile_n, M, monkeypatch):
-    monkeypatch.setenv("GRINQH_PREFILL_TILE", tile)
+def test_prefill_tile_configs(g, torch, tile, K, N, levels, tile_n, M, opts):
+    opts(g.GRINQH_OPT_PREFILL_TILE, int(tile) + 1)
     L = Layer(g, torch, K, N, levels, cfg=64, layer=K + M, tile_n=tile_n)
     x = inputs.activations_t3(K, M, 64, K + M)
     y = _host(g.grinqh_prefill(L.desc, L.pc, L.ps, _dev(torch, x)))
@@ -651,9 +664,9 @@ def test_pack_bmax_bit_exact(g, torch, levels, codes_src):
 
 @pytest.mark.parametrize("levels", BMAX_LEVELS)
 @pytest.mark.parametrize("kernel", ["auto", "dot2", "v0"])
-def test_vmm_bmax_random_level_maps(g, torch, levels, kernel, monkeypatch):
+def test_vmm_bmax_random_level_maps(g, torch, levels, kernel, opts):
     if kernel != "auto":
-        monkeypatch.setenv("GRINQH_VMM_KERNEL", kernel)
+        opts(g.GRINQH_OPT_VMM_KERNEL, KERNEL[kernel])
     K, N = 1152, 1024
     L = Layer(g, torch, K, N, levels, cfg=81, codes_src=True)
     rng = np.random.default_rng(81)
@@ -690,8 +703,8 @@ def test_vmm_bmax_topk_and_threshold(g, torch, levels):
 
 @pytest.mark.parametrize("levels", BMAX_LEVELS)
 @pytest.mark.parametrize("tile", ["0", "1", "2"])
-def test_prefill_bmax(g, torch, levels, tile, monkeypatch):
-    monkeypatch.setenv("GRINQH_PREFILL_TILE", tile)
+def test_prefill_bmax(g, torch, levels, tile, opts):
+    opts(g.GRINQH_OPT_PREFILL_TILE, int(tile) + 1)
     K, N, M = 384, 1024, 200
     L = Layer(g, torch, K, N, levels, cfg=83, layer=int(tile), tile_n=512)
     x = inputs.activations_t3(K, M, 83, int(tile))
@@ -791,9 +804,9 @@ def test_vmm_lut_with_uniform_tables_is_the_uniform_vmm(g, torch, levels):
     assert normwise(y_lut, orc.vmm_batch(L.codes, np.ascontiguousarray(sc_nk.T), x, lm, levels)) <= TOL
 
 
-@pytest.mark.parametrize("gps", ["1", "3", "32"])
-def test_vmm_lut_full_size_topk(g, torch, gps, monkeypatch):
-    monkeypatch.setenv("GRINQH_LUT_GPS", gps)
+@pytest.mark.parametrize("gps", ["1", "3", "16"])
+def test_vmm_lut_full_size_topk(g, torch, gps, opts):
+    opts(g.GRINQH_OPT_LUT_GROUPS, gps)
     K, N, levels = 4096, 4096, inputs.LEVELS_B
     L = LutLayer(g, torch, K, N, levels, layer=4)
     x = inputs.activations_t3(K, 1, 92, 0)
@@ -818,10 +831,10 @@ def test_vmm_lut_accumulate(g, torch):
 
 @pytest.mark.parametrize("levels", [(0, 2, 3, 4, 8), (0, 1, 2, 3, 4), (0, 3, 6)])
 @pytest.mark.parametrize("tile_n", [512, 1024])
-def test_vmm_one_bit_planes_dot2(g, torch, levels, tile_n, monkeypatch):
+def test_vmm_one_bit_planes_dot2(g, torch, levels, tile_n, opts):
     # 1-bit planes through the per-plane kernel: each plane a work item at
     # its own weight, per-token depths exact for B > 1
-    monkeypatch.setenv("GRINQH_VMM_KERNEL", "dot2")
+    opts(g.GRINQH_OPT_VMM_KERNEL, g.GRINQH_KERNEL_PER_PLANE)
     K, N = 1152, 2048
     L = Layer(g, torch, K, N, levels, cfg=84, layer=tile_n, tile_n=tile_n)
     assert L.desc.plane_bits == 1
