@@ -144,6 +144,17 @@ GRINQH_API int grinqh_calibrate(const grinqh_layer_desc* desc, const void* x, in
                                 const int32_t* p_bp, double* per_sample, float* theta,
                                 void* stream);
 
+/* grinqh_calibrate for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
+ * the per-sample scratch lives in a static device array of the library
+ * (1 MiB, float64, each GPU holds its own until the process ends), so the
+ * caller passes no workspace.  Arguments and result as grinqh_calibrate;
+ * S * (n_levels - 1) must not exceed 131072 (GRINQH_ESIZE otherwise).  No
+ * entry point here allocates; calls that overlap on one GPU share the
+ * scratch and race, so keep them in one stream (or serialise them). */
+GRINQH_API int grinqh_calibrate_noalloc(const grinqh_layer_desc* desc, const void* x, int32_t S,
+                                        const int32_t* p_bp, float* theta, void* stream);
+
 /* Per-token precision assignment (Sec. 3.1; App. A.1).
  *   x: fp16 [B][K] (device), finite.
  *   mode GRINQH_ASSIGN_THRESHOLD: thresholds = host fp32 theta_1..theta_n

@@ -1,5 +1,7 @@
 // Per-token precision assignment (Sec. 3.1 threshold grading; App. A.1 top-p
 // partition of |x| into the fractions P).
+#include <mutex>
+
 #include "grinqh_internal.h"
 
 namespace grinqh {
@@ -320,6 +322,49 @@ int launch_calibrate(const Layer& L, const void* x, int S, const QuantilePos& qp
   if (st) return st;
   hipLaunchKernelGGL(k_calibrate_mean, dim3(1), dim3(64), 0, s, per_sample, S, qp.n, theta);
   return check_launch("calibrate (mean)");
+}
+
+// Scratch of grinqh_calibrate_noalloc: the per-sample thresholds, float64
+// [S][n] with S * n <= kCalibScratch, in a static array each GPU holds for
+// the life of the process.  Host code never names the array in a launch or a
+// copy: its device address comes from hipGetSymbolAddress, once per device,
+// with that device current.  Every entry the mean reads is written by the
+// sample kernel of the same call first, so nothing needs clearing; calls that
+// overlap on one GPU share the array and race.
+static __device__ __align__(256) double scratch[kCalibScratch];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+double* g_scratch_ptr[kMaxDevices] = {};
+}  // namespace
+
+static int scratch_ptr(double** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(GRINQH_EHIP, "calibrate (no-alloc): hipGetDevice: %s", hipGetErrorString(e));
+  if (dev < 0 || dev >= kMaxDevices) return fail(GRINQH_EUNSUPPORTED, "calibrate (no-alloc): device %d beyond %d", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p)
+      return fail(GRINQH_EHIP, "calibrate (no-alloc): hipGetSymbolAddress: %s", hipGetErrorString(e));
+    g_scratch_ptr[dev] = (double*)p;
+  }
+  *out = g_scratch_ptr[dev];
+  return GRINQH_OK;
+}
+
+int launch_calibrate_noalloc(const Layer& L, const void* x, int S, const QuantilePos& qp,
+                             float* theta, hipStream_t s) {
+  if ((long)S * qp.n > kCalibScratch)
+    return fail(GRINQH_ESIZE, "calibrate (no-alloc): S*n = %ld per-sample thresholds exceed the %d of the static scratch",
+                (long)S * qp.n, kCalibScratch);
+  double* per_sample = nullptr;
+  const int st = scratch_ptr(&per_sample);
+  if (st) return st;
+  return launch_calibrate(L, x, S, qp, per_sample, theta, s);
 }
 
 int launch_assign_threshold(const Layer& L, const void* x, int B, const Thresholds& th,

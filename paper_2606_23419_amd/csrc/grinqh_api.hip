@@ -185,37 +185,57 @@ int grinqh_workspace_bytes(const grinqh_layer_desc* desc, int32_t B, size_t* byt
   return GRINQH_OK;
 }
 
-int grinqh_calibrate(const grinqh_layer_desc* desc, const void* x, int32_t S, const int32_t* p_bp,
-                     double* per_sample, float* theta, void* stream) {
-  clear_error();
-  Layer L;
-  int st = resolve(desc, &L, nullptr);
+// Validation shared by both calibration entry points, and the quantile
+// positions h = (K-1) U_k / 10000 taken exactly: lo = floor(h), frac its
+// fraction.
+static int calibrate_checks(const grinqh_layer_desc* desc, const void* x, int32_t S,
+                            const int32_t* p_bp, float* theta, Layer* L, QuantilePos* qp) {
+  int st = resolve(desc, L, nullptr);
   if (st) return st;
-  if (!x || !p_bp || !per_sample || !theta)
-    return fail(GRINQH_EINVAL, "x, p_bp, per_sample and theta must not be NULL");
+  if (!x || !p_bp || !theta) return fail(GRINQH_EINVAL, "x, p_bp and theta must not be NULL");
   if (S < 1 || S > 65535) return fail(GRINQH_EINVAL, "S=%d outside 1..65535", S);
-  if (L.K > 16384) return fail(GRINQH_EUNSUPPORTED, "calibration needs K <= 16384 (K=%d)", L.K);
+  if (L->K > 16384) return fail(GRINQH_EUNSUPPORTED, "calibration needs K <= 16384 (K=%d)", L->K);
   if ((uintptr_t)x & 3u) return fail(GRINQH_EINVAL, "x must be 4-byte aligned");
-  if ((uintptr_t)per_sample & 7u) return fail(GRINQH_EINVAL, "per_sample must be 8-byte aligned");
   if ((uintptr_t)theta & 3u) return fail(GRINQH_EINVAL, "theta must be 4-byte aligned");
   long long total = 0;
-  for (int j = 0; j < L.n_levels; ++j) {
+  for (int j = 0; j < L->n_levels; ++j) {
     if (p_bp[j] < 0) return fail(GRINQH_EINVAL, "p_bp[%d]=%d is negative", j, p_bp[j]);
     total += p_bp[j];
   }
   if (total != 10000) return fail(GRINQH_EINVAL, "p_bp sums to %lld, not 10000", total);
-  // h = (K-1) U_k / 10000 taken exactly: lo = floor(h), frac = its fraction
-  QuantilePos qp{};
-  qp.n = L.n_levels - 1;
+  *qp = QuantilePos{};
+  qp->n = L->n_levels - 1;
   long long U = 0;
-  for (int k = 0; k < qp.n; ++k) {
+  for (int k = 0; k < qp->n; ++k) {
     U += p_bp[k];
-    const long long num = (long long)(L.K - 1) * U;
-    qp.lo[k] = (int)(num / 10000);
-    qp.hi[k] = qp.lo[k] + 1 < L.K ? qp.lo[k] + 1 : L.K - 1;
-    qp.frac[k] = (double)(num % 10000) / 10000.0;
+    const long long num = (long long)(L->K - 1) * U;
+    qp->lo[k] = (int)(num / 10000);
+    qp->hi[k] = qp->lo[k] + 1 < L->K ? qp->lo[k] + 1 : L->K - 1;
+    qp->frac[k] = (double)(num % 10000) / 10000.0;
   }
+  return GRINQH_OK;
+}
+
+int grinqh_calibrate(const grinqh_layer_desc* desc, const void* x, int32_t S, const int32_t* p_bp,
+                     double* per_sample, float* theta, void* stream) {
+  clear_error();
+  if (!per_sample) return fail(GRINQH_EINVAL, "per_sample must not be NULL");
+  if ((uintptr_t)per_sample & 7u) return fail(GRINQH_EINVAL, "per_sample must be 8-byte aligned");
+  Layer L;
+  QuantilePos qp;
+  int st = calibrate_checks(desc, x, S, p_bp, theta, &L, &qp);
+  if (st) return st;
   return launch_calibrate(L, x, S, qp, per_sample, theta, (hipStream_t)stream);
+}
+
+int grinqh_calibrate_noalloc(const grinqh_layer_desc* desc, const void* x, int32_t S,
+                             const int32_t* p_bp, float* theta, void* stream) {
+  clear_error();
+  Layer L;
+  QuantilePos qp;
+  int st = calibrate_checks(desc, x, S, p_bp, theta, &L, &qp);
+  if (st) return st;
+  return launch_calibrate_noalloc(L, x, S, qp, theta, (hipStream_t)stream);
 }
 
 int grinqh_assign(const grinqh_layer_desc* desc, int mode, const void* x, int32_t B,

@@ -95,6 +95,10 @@ int launch_assign_topk(const Layer& L, const void* x, int B, const TopkCuts& cut
                        uint8_t* level_map, hipStream_t s);
 int launch_calibrate(const Layer& L, const void* x, int S, const QuantilePos& qp,
                      double* per_sample, float* theta, hipStream_t s);
+// float64 entries of the static per-sample scratch of grinqh_calibrate_noalloc
+constexpr int kCalibScratch = 1 << 17;   // 1 MiB
+int launch_calibrate_noalloc(const Layer& L, const void* x, int S, const QuantilePos& qp,
+                             float* theta, hipStream_t s);
 bool vmm_pp_supported(const Layer& L, int B);
 int launch_vmm_pp(const Layer& L, const void* codes, const void* scales, const void* x,
                   const uint8_t* level_map, const Thresholds* th, uint8_t* level_map_out,

@@ -38,7 +38,8 @@ EXPORTED = (
     "grinqh_resolve_desc", "grinqh_packed_bytes", "grinqh_pack", "grinqh_topk_counts",
     "grinqh_workspace_bytes", "grinqh_calibrate", "grinqh_assign", "grinqh_vmm",
     "grinqh_vmm_threshold", "grinqh_prefill", "grinqh_lut_entries", "grinqh_vmm_lut",
-    "grinqh_vmm_lut_threshold", "grinqh_set_option", "grinqh_last_error",
+    "grinqh_vmm_lut_threshold", "grinqh_set_option", "grinqh_calibrate_noalloc",
+    "grinqh_last_error",
 )
 
 
@@ -88,6 +89,7 @@ def _load():
         "grinqh_vmm_lut": [dp, vp, vp, vp, vp, i32, vp, i32, vp],
         "grinqh_vmm_lut_threshold": [dp, vp, vp, vp, i32, ctypes.POINTER(ctypes.c_float), vp, vp, i32, vp],
         "grinqh_set_option": [ctypes.c_int, ctypes.c_int],
+        "grinqh_calibrate_noalloc": [dp, vp, i32, ctypes.POINTER(i32), vp, vp],
     }
     for name, args in sig.items():
         f = getattr(lib, name)
@@ -241,6 +243,24 @@ def grinqh_calibrate(desc: LayerDesc, x, p_bp, per_sample=None, theta=None, stre
     tp = _dev(theta, torch.float32, "theta", (n,))
     arr = _host_array([int(v) for v in p_bp], rd.n_levels, ctypes.c_int32, "p_bp")
     _check(lib.grinqh_calibrate(ctypes.byref(rd), xp, S, arr, pp, tp, _stream(stream)))
+    return theta
+
+
+def grinqh_calibrate_noalloc(desc: LayerDesc, x, p_bp, theta=None, stream=None):
+    """grinqh_calibrate with the library's static scratch: no workspace is
+    passed (theta is allocated here only when the caller passes none)."""
+    torch = _torch()
+    rd = grinqh_resolve_desc(desc)
+    if x.dim() == 1:
+        x = x.view(1, -1)
+    S = int(x.shape[0])
+    n = rd.n_levels - 1
+    xp = _dev(x, torch.float16, "x", (S, rd.K))
+    if theta is None:
+        theta = torch.empty((n,), dtype=torch.float32, device=x.device)
+    tp = _dev(theta, torch.float32, "theta", (n,))
+    arr = _host_array([int(v) for v in p_bp], rd.n_levels, ctypes.c_int32, "p_bp")
+    _check(lib.grinqh_calibrate_noalloc(ctypes.byref(rd), xp, S, arr, tp, _stream(stream)))
     return theta
 
 
