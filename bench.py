@@ -1,10 +1,10 @@
 """Benchmark of the nested-precision decode VMM on one MI355X.
 
-Default workload: the Llama3-8B attention projections at batch 1, 256
-synthetic tokens, average budget 4 bits over the levels {0,2,4,6,8}.  The
-q, k and v projections (4096x4096, 4096->1024, 4096->1024) share their input
-and run as one merged 4096->6144 projection, as serving engines store them;
-then the o projection (4096x4096).
+Default workload (`python bench.py`): the whole decode step of a 32-layer
+Llama3-8B-shaped model at batch 1, average budget 4 bits over the levels
+{0,2,4,6,8}: per layer the merged q|k|v projection (4096->6144), o
+(4096x4096), the merged gate|up projection (4096->28672) and down
+(14336->4096), 128 VMM launches per token over 7.1 GB of packed weights.
 
 Assignment modes (--assign):
   threshold  the runtime form: per-layer thresholds calibrated offline on a
@@ -15,17 +15,21 @@ Assignment modes (--assign):
 The default is threshold; the JSON line also carries the top-k step.
 
 One step is the whole hot path for every token, captured once as a HIP graph
-and replayed.  The packed weights rotate over enough distinct copies
-(> 512 MiB) that the 256 MiB last-level cache cannot serve them between uses.
+and replayed; each launch reads its own layer's weights, so nothing is served
+from the 256 MiB last-level cache.  (The single-layer workloads rotate over
+more than 512 MiB of weight copies for the same reason.)
 
 Output: one JSON line.  `value` is whole-step throughput in GB/s of required
 bytes (sum over every VMM of the bytes its level map requires: code prefixes,
 scales of groups with an active channel, x, y, and the level map where one is
-read); `roofline` is for the VMM kernel alone, timed with HIP events on its
-own stream.  With --bits-sweep, `vs_bits` repeats the VMM-only timing at
-every average-bit budget of the level set (thresholds calibrated per budget):
-µs per VMM, GB/s of required bytes and the fraction of the HBM peak against
-average bits.
+read).  `roofline` is for the VMM kernel alone: the required bytes of the
+step's VMM launches over the time of a graph of those launches, timed with
+HIP events on the stream they run on, against the 8 TB/s HBM peak and a
+measured streaming-read ceiling; `traffic` is the HBM bytes per launch from
+a committed rocprofv3 FETCH_SIZE/WRITE_SIZE summary of the same workload.
+`vs_bits` times the step at 2, 3 and 4 average bits, `per_layer` each
+projection's launches alone, and `cpu_baseline` the CPU oracle on a bounded
+sample of the step.
 """
 from __future__ import annotations
 
@@ -154,9 +158,9 @@ def workload(name: str, bmax: int):
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="llama3-8b-attn", choices=sorted(WORKLOADS))
+    ap.add_argument("--workload", default="llama3-8b-decode", choices=sorted(WORKLOADS))
     ap.add_argument("--assign", default="threshold", choices=("threshold", "topk"))
     ap.add_argument("--budget", type=int, default=None, help="override the average-bit budget")
     ap.add_argument("--tokens", type=int, default=256)
@@ -172,6 +176,9 @@ def parse():
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
     ap.add_argument("--vmm-only-reps", type=int, default=5)
     ap.add_argument("--no-ref", action="store_true", help="skip the reference-shape timings")
+    ap.add_argument("--no-bits-sweep", action="store_true",
+                    help="decode workload: skip the 2/3/4-bit timing of the step (vs_bits)")
+    ap.add_argument("--no-stream", action="store_true", help="skip the measured streaming-read ceiling")
     ap.add_argument("--bits-sweep", action="store_true",
                     help="also time the VMM launches at every budget of the level set (vs_bits); off by "
                          "default so that a kernel trace of the default run covers the one workload")
@@ -244,6 +251,93 @@ def cpu_baseline(wl, p_bp, assign: str, tokens_sample: int):
                       f"same workload, numpy float64, 1 thread; {dt:.1f} s"}
 
 
+def cpu_info():
+    """Host CPU model and the cores this process may run on."""
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return model, len(os.sched_getaffinity(0))
+
+
+def cpu_baseline_decode(wl, thresholds_host, layers_sample, tokens_sample: int):
+    """Time the oracle (threshold assignment + dequantise + float64 matvec) on
+    a bounded sample of the decode step: `tokens_sample` tokens through the
+    named projections of one layer, once on every host core the process may
+    use and once on one thread.  Codes and scales are uniform random like the
+    GPU weights (numpy draws of the same distribution)."""
+    from threadpoolctl import threadpool_limits
+    from oracle import grinqh_oracle as orc
+
+    levels = wl["levels"]
+    bmax = int(levels[-1])
+    xs = make_inputs(wl, tokens_sample, 100)
+    sample = [l for l in wl["layers"] if l[0] in layers_sample]
+    weights = {}
+    for li, (name, K, N, _, _) in enumerate(sample):
+        codes = inputs.random_codes(N, K, wl["cfg"], li)
+        if bmax < 8:
+            codes = (codes & ((1 << bmax) - 1)).astype(np.uint8)
+        weights[name] = (codes, np.ascontiguousarray(inputs.random_scales(N, K, 128, wl["cfg"], li).T))
+    model, ncores = cpu_info()
+    runs = {}
+    for threads in (ncores, 1):
+        total_bytes, dt = 0, 0.0
+        with threadpool_limits(limits=threads):
+            for t in range(tokens_sample):
+                for name, K, N, xin, _ in sample:
+                    t0 = time.perf_counter()
+                    lm = orc.assign_threshold(xs[xin][t], thresholds_host[xin])
+                    q, sc = weights[name]
+                    orc.vmm(q, sc, xs[xin][t], lm, levels)
+                    dt += time.perf_counter() - t0
+                    total_bytes += int(bytes_required(lm[None, :], levels, K, N, False)[0])
+        runs[threads] = (total_bytes / dt / 1e9, dt)
+    all_gbs, all_s = runs[ncores]
+    one_gbs, one_s = runs[1]
+    names = ", ".join(layers_sample)
+    return {"value": round(all_gbs, 4), "unit": "GB/s", "cores": ncores, "kind": "oracle",
+            "sample": f"{tokens_sample} token(s) x one layer's {names} projections of the 32-layer step "
+                      f"(the same 4 merged VMMs each layer runs; GB/s of required bytes does not change "
+                      f"with the layer count), numpy float64 threshold assignment + dequantise + matvec; "
+                      f"{all_s:.1f} s on {ncores} cores",
+            "ms_per_token_extrapolated_x32": round(32 * 1e3 * all_s / tokens_sample, 1)
+            if len(layers_sample) == len(wl["layers"]) else None,
+            "single_thread": {"value": round(one_gbs, 4), "unit": "GB/s", "cores": 1,
+                              "seconds": round(one_s, 1)},
+            "cpu_model": model,
+            "note": "the oracle is a correctness reference, not a tuned CPU kernel"}
+
+
+def stream_ceiling(torch, g, reps: int = 10):
+    """Measured streaming-read ceiling: grinqh_stream_read over 1 GiB (four
+    times the last-level cache), timed with HIP events."""
+    buf = torch.ones(1 << 30, dtype=torch.uint8, device="cuda")
+    sink = torch.zeros(1, dtype=torch.int32, device="cuda")
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        g.grinqh_stream_read(buf, sink, stream=s)
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(s)
+        for _ in range(reps):
+            g.grinqh_stream_read(buf, sink, stream=s)
+        b.record(s)
+    torch.cuda.synchronize()
+    ms = a.elapsed_time(b) / reps
+    del buf
+    return round(buf_bytes_gbs(1 << 30, ms), 1)
+
+
+def buf_bytes_gbs(nbytes, ms):
+    return nbytes / (ms * 1e-3) / 1e9
+
+
 def run_decode(args, torch, g):
     """The full decode step: n_layers x (qkv, o, gate_up, down) at batch B.
 
@@ -280,9 +374,14 @@ def run_decode(args, torch, g):
         weights.append(per)
     torch.cuda.synchronize()
     xs = {k: torch.from_numpy(v[:B].copy()).to(dev) for k, v in make_inputs(wl, B, 100).items()}
-    calib = {k: torch.from_numpy(v).to(dev) for k, v in make_inputs(wl, CALIB_TOKENS, 200).items()}
+    calib_host = make_inputs(wl, CALIB_TOKENS, 200)
+    calib = {k: torch.from_numpy(v).to(dev) for k, v in calib_host.items()}
     desc_of = {xin: descs[name] for name, _, _, xin, _ in layers}
-    thresholds = {xin: g.grinqh_calibrate(desc_of[xin], calib[xin], p_bp).cpu().numpy() for xin in xs}
+
+    def thresholds_for(pb):
+        return {xin: g.grinqh_calibrate(desc_of[xin], calib[xin], pb).cpu().numpy() for xin in xs}
+
+    thresholds = thresholds_for(p_bp)
     counts = {xin: g.grinqh_topk_counts(int(xs[xin].shape[1]), p_bp) for xin in xs}
     lm = {xin: torch.zeros((B, int(x.shape[1])), dtype=torch.uint8, device=dev) for xin, x in xs.items()}
     # The step's outputs live in one buffer, cleared once per step (one fill
@@ -302,13 +401,14 @@ def run_decode(args, torch, g):
         out.append(per)
     ys = out[L - 1]
 
-    def step(mode):
-        arena.zero_()
+    def vmm_calls(mode, th, only=None):
         for li in range(L):
             w = weights[li]
             for name, K, N, xin, _ in layers:
+                if only is not None and name != only:
+                    continue
                 if mode == "threshold":
-                    g.grinqh_vmm_threshold(descs[name], w[name][0], w[name][1], xs[xin], thresholds[xin],
+                    g.grinqh_vmm_threshold(descs[name], w[name][0], w[name][1], xs[xin], th[xin],
                                            y=out[li][name], level_map_out=lm[xin] if li == 0 else None,
                                            accumulate=True)
                 else:
@@ -317,18 +417,51 @@ def run_decode(args, torch, g):
                     g.grinqh_vmm(descs[name], w[name][0], w[name][1], xs[xin], lm[xin], y=out[li][name],
                                  accumulate=True)
 
+    def step(mode, th):
+        arena.zero_()
+        vmm_calls(mode, th)
+
     s = torch.cuda.Stream()
     s.wait_stream(torch.cuda.current_stream())
+
+    def capture(fn):
+        gr = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(gr, stream=s):
+            fn()
+        return gr
+
+    def timed(gr, reps, warm=2, per_rep=False):
+        with torch.cuda.stream(s):
+            for _ in range(warm):
+                gr.replay()
+        torch.cuda.synchronize()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(reps + 1)]
+        with torch.cuda.stream(s):
+            ev[0].record(s)
+            for i in range(reps):
+                gr.replay()
+                if per_rep:
+                    ev[i + 1].record(s)
+            if not per_rep:
+                ev[reps].record(s)
+        torch.cuda.synchronize()
+        total = ev[0].elapsed_time(ev[reps]) / reps
+        if not per_rep:
+            return total
+        return total, [ev[i].elapsed_time(ev[i + 1]) for i in range(reps)]
+
+    def step_bytes_of(lm_host, mode):
+        return L * sum(bytes_required_batch(lm_host[xin], levels, K, N, mode == "topk")
+                       for _, K, N, xin, _ in layers)
+
     out_modes = {}
     for mode in (args.assign, "topk" if args.assign == "threshold" else "threshold"):
         with torch.cuda.stream(s):
-            step(mode)
+            step(mode, thresholds)
         torch.cuda.synchronize()
         eager = {n: y.clone() for n, y in ys.items()}
         lm_host = {xin: m.cpu().numpy() for xin, m in lm.items()}
-        gr = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(gr, stream=s):
-            step(mode)
+        gr = capture(lambda: step(mode, thresholds))
         with torch.cuda.stream(s):
             gr.replay()
         torch.cuda.synchronize()
@@ -336,31 +469,62 @@ def run_decode(args, torch, g):
             err = float((y - eager[n]).abs().max() / eager[n].abs().max())
             if not err <= 1e-5:
                 raise RuntimeError(f"graph replay of {n} ({mode}) differs from the eager step ({err:.2e})")
-        step_bytes = L * sum(bytes_required_batch(lm_host[xin], levels, K, N, mode == "topk")
-                             for _, K, N, xin, _ in layers)
-        reps = args.steps if mode == args.assign else 3
-        with torch.cuda.stream(s):
-            for _ in range(args.warmup):
-                gr.replay()
-        torch.cuda.synchronize()
-        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        with torch.cuda.stream(s):
-            a.record(s)
-            for _ in range(reps):
-                gr.replay()
-            b.record(s)
-        torch.cuda.synchronize()
-        ms = a.elapsed_time(b) / reps
+        step_bytes = step_bytes_of(lm_host, mode)
+        if mode == args.assign:
+            ms, per_rep = timed(gr, args.steps, args.warmup, per_rep=True)
+        else:
+            ms, per_rep = timed(gr, 5), None
         out_modes[mode] = {"ms_per_step": round(ms, 4), "step_bytes": step_bytes,
                            "value": round(step_bytes / (ms * 1e-3) / 1e9, 2),
                            "achieved_avg_bits": {f"input{xin}": round(float(np.asarray(levels)[m].mean()), 4)
-                                                 for xin, m in lm_host.items()}}
+                                                 for xin, m in lm_host.items()},
+                           "lm_host": lm_host, "per_rep": per_rep}
         del gr
     main = out_modes[args.assign]
     other = "topk" if args.assign == "threshold" else "threshold"
     n_vmm = L * len(layers)
+
+    # the VMM launches alone (no arena fill): the kernel's achieved bandwidth
+    gv = capture(lambda: vmm_calls(args.assign, thresholds))
+    ms_vmm = timed(gv, max(5, args.steps))
+    del gv
+    achieved = main["step_bytes"] / (ms_vmm * 1e-3) / 1e9
+    # each projection's 32 launches alone
+    per_layer = {}
+    if args.assign == "threshold":
+        for name, K, N, xin, _ in layers:
+            gl = capture(lambda: vmm_calls("threshold", thresholds, only=name))
+            ms_l = timed(gl, 10)
+            del gl
+            req = bytes_required_batch(main["lm_host"][xin], levels, K, N, False)
+            per_layer[name] = {"K": K, "N": N, "tile_n": int(descs[name].tile_n),
+                               "us_per_vmm": round(ms_l * 1e3 / L, 3), "required_bytes": int(req),
+                               "GBps": round(req * L / (ms_l * 1e-3) / 1e9, 1)}
+    # time against average bits: the whole step's VMM launches per budget
+    vs_bits = {}
+    if args.assign == "threshold" and not args.no_bits_sweep:
+        for bb in (2, 3, 4):
+            if bb not in inputs.BUDGETS[levels]:
+                continue
+            th_b = thresholds_for(inputs.BUDGETS[levels][bb])
+            with torch.cuda.stream(s):
+                step("threshold", th_b)
+            torch.cuda.synchronize()
+            lmh = {xin: m.cpu().numpy() for xin, m in lm.items()}
+            sb = step_bytes_of(lmh, "threshold")
+            gb = capture(lambda: vmm_calls("threshold", th_b))
+            ms_b = timed(gb, max(5, args.steps))
+            del gb
+            gbs = sb / (ms_b * 1e-3) / 1e9
+            vs_bits[str(bb)] = {"achieved_avg_bits": round(float(np.mean([np.asarray(levels)[m].mean()
+                                                                          for m in lmh.values()])), 3),
+                                "ms_per_token": round(ms_b / B, 4), "us_per_vmm": round(ms_b * 1e3 / n_vmm, 3),
+                                "step_bytes": int(sb), "GBps": round(gbs, 1), "frac": round(gbs / HBM_PEAK_GBS, 4)}
+    ceiling = None if args.no_stream else stream_ceiling(torch, g)
     packed_gb = sum(w[n][0].numel() + 2 * w[n][1].numel() for w in weights for n in w) / 1e9
-    out = {
+    traffic = stored_traffic(wl_name, budget, args.assign) if (B == 1 and L == wl["n_layers"]) else None
+    per_rep = np.asarray(main["per_rep"])
+    res = {
         "metric": "µs per decode VMM and effective HBM GB/s (% of peak) vs avg bits, batch 1",
         "value": main["value"], "unit": "GB/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": main["ms_per_step"], "higher_is_better": True, "scaling": "weak",
@@ -373,14 +537,24 @@ def run_decode(args, torch, g):
                    "outputs": "one buffer per step, cleared by one fill, VMMs accumulate",
                    "packed_weights_GB": round(packed_gb, 3), "achieved_avg_bits": main["achieved_avg_bits"]},
         "tokens_per_s": round(B / (main["ms_per_step"] * 1e-3), 1),
-        "ms_per_token_step": main["ms_per_step"],
-        "us_per_vmm": round(main["ms_per_step"] * 1e3 / n_vmm, 3),
-        "roofline": {"bound": "hbm", "achieved": main["value"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(main["value"] / HBM_PEAK_GBS, 4), "traffic": None},
+        "ms_per_token": round(main["ms_per_step"] / B, 4),
+        "ms_per_step_p10_p50_p90": [round(float(np.percentile(per_rep, q)), 4) for q in (10, 50, 90)],
+        "us_per_vmm": round(ms_vmm * 1e3 / n_vmm, 3),
+        "algorithmic_bytes_per_vmm": round(main["step_bytes"] / n_vmm, 1),
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
+                     "kernel": "k_vmm_sr (every VMM launch of the step), HIP events over a graph of them",
+                     **({"measured_read_ceiling": ceiling,
+                         "frac_of_measured_ceiling": round(achieved / ceiling, 4)} if ceiling else {})},
+        "per_layer": per_layer,
+        **({"vs_bits": vs_bits} if vs_bits else {}),
         "other_assignment": dict(assignment=other, **{k: v for k, v in out_modes[other].items()
-                                                       if k != "step_bytes"}),
+                                                       if k not in ("step_bytes", "lm_host", "per_rep")}),
     }
-    print(json.dumps(out), flush=True)
+    if not args.no_cpu and B == 1:
+        res["cpu_baseline"] = cpu_baseline_decode(wl, {xin: t for xin, t in thresholds.items()},
+                                                  ("qkv", "o", "gate_up", "down"), tokens_sample=1)
+    print(json.dumps(res), flush=True)
 
 
 def cpu_baseline_prefill(wl, tokens_sample: int):

@@ -262,6 +262,14 @@ GRINQH_API int grinqh_vmm_lut_threshold(const grinqh_layer_desc* desc, const voi
  * setting is read when a call enqueues its kernels; set it between calls. */
 GRINQH_API int grinqh_set_option(int option, int value);
 
+/* Measurement infrastructure, not an operation of the paper: read `bytes` of
+ * device memory at src (16-byte aligned; a positive multiple of 2 MiB) with
+ * non-temporal 16-byte loads, eight in flight per lane, as fast as the chip
+ * streams them, and XOR a fold of the data into *sink (device uint32).  It
+ * gives the measured streaming-read ceiling the VMM's bandwidth is compared
+ * with. */
+GRINQH_API int grinqh_stream_read(const void* src, size_t bytes, uint32_t* sink, void* stream);
+
 /* Infrastructure, not an operation of the paper: the message of the last
  * failing call on this thread ("" if none), valid until that thread's next
  * call. */

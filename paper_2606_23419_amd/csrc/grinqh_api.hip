@@ -409,6 +409,15 @@ int grinqh_set_option(int opt, int value) {
   return GRINQH_OK;
 }
 
+int grinqh_stream_read(const void* src, size_t bytes, uint32_t* sink, void* stream) {
+  clear_error();
+  if (!src || !sink) return fail(GRINQH_EINVAL, "src and sink must not be NULL");
+  if (((uintptr_t)src & 15u) || ((uintptr_t)sink & 3u)) return fail(GRINQH_EINVAL, "src must be 16-byte and sink 4-byte aligned");
+  if (bytes == 0 || bytes % (2u << 20) || bytes / 512 > 0xFFFFFFFFull)
+    return fail(GRINQH_EINVAL, "bytes=%zu must be a positive multiple of 2 MiB below 2 TiB", bytes);
+  return launch_stream_read(src, bytes, sink, (hipStream_t)stream);
+}
+
 const char* grinqh_last_error(void) { return g_err; }
 
 }  // extern "C"

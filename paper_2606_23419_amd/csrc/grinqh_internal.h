@@ -113,6 +113,7 @@ int launch_vmm(const Layer& L, const void* codes, const void* scales, const void
 int launch_prefill(const Layer& L, const void* codes, const void* scales, const void* x, int M,
                    float* y, int accumulate, hipStream_t s);
 int lut_desc(const Layer& L, LutDesc* D);
+int launch_stream_read(const void* src, size_t bytes, uint32_t* sink, hipStream_t s);
 // level_map == nullptr with th != nullptr: levels graded from x in the kernel,
 // written to level_map_out if that is not null
 int launch_vmm_lut(const Layer& L, const void* codes, const void* luts, const void* x,

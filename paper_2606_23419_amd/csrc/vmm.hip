@@ -103,6 +103,47 @@ __global__ __launch_bounds__(kVmmThreads) void k_vmm_v0(
   }
 }
 
+// Streaming read for the measured read ceiling (measurement infrastructure):
+// workgroup b reads bytes [b*chunk, (b+1)*chunk) in 16-byte pieces per lane,
+// eight loads in flight, and folds them with XOR; each wave leaves its fold
+// in sink with one atomic XOR so the loads cannot be dropped.
+constexpr int kStreamThreads = 256, kStreamRing = 8;
+
+__global__ __launch_bounds__(kStreamThreads) void k_stream_read(const uint8_t* __restrict__ src,
+                                                               uint32_t chunk, int n_it,
+                                                               uint32_t* __restrict__ sink) {
+  typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+  constexpr int STEP = kStreamThreads * 16;
+  const uint8_t* p = src + (size_t)blockIdx.x * chunk + threadIdx.x * 16;
+  u32x4 r[kStreamRing];
+  uint32_t acc = 0u;
+#pragma unroll
+  for (int i = 0; i < kStreamRing - 1; ++i)
+    r[i] = __builtin_nontemporal_load((const u32x4*)(p + (size_t)min(i, n_it - 1) * STEP));
+  for (int it = 0; it < n_it; it += kStreamRing) {
+#pragma unroll
+    for (int i = 0; i < kStreamRing; ++i) {
+      const int j = min(it + i + kStreamRing - 1, n_it - 1);
+      r[(i + kStreamRing - 1) % kStreamRing] = __builtin_nontemporal_load((const u32x4*)(p + (size_t)j * STEP));
+      if (it + i < n_it) acc ^= r[i].x ^ r[i].y ^ r[i].z ^ r[i].w;
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+  for (int o = 32; o > 0; o >>= 1) acc ^= (uint32_t)__shfl_xor((int)acc, o);
+  if ((threadIdx.x & 63) == 0) atomicXor(sink, acc);
+}
+
+int launch_stream_read(const void* src, size_t bytes, uint32_t* sink, hipStream_t s) {
+  // 512 workgroups, each a contiguous chunk of bytes / 512 (a multiple of
+  // 4 KiB below 4 GiB: the caller passes a multiple of 2 MiB below 2 TiB)
+  constexpr size_t kStep = (size_t)kStreamThreads * 16;
+  constexpr int nwg = 512;
+  const size_t chunk = bytes / nwg;
+  hipLaunchKernelGGL(k_stream_read, dim3((unsigned)nwg), dim3(kStreamThreads), 0, s,
+                     (const uint8_t*)src, (uint32_t)chunk, (int)(chunk / kStep), sink);
+  return check_launch("stream read");
+}
+
 int launch_vmm(const Layer& L, const void* codes, const void* scales, const void* x,
                const uint8_t* level_map, const Thresholds* th, uint8_t* level_map_out,
                int B, float* y, int accumulate, hipStream_t s) {

@@ -39,7 +39,7 @@ EXPORTED = (
     "grinqh_workspace_bytes", "grinqh_calibrate", "grinqh_assign", "grinqh_vmm",
     "grinqh_vmm_threshold", "grinqh_prefill", "grinqh_lut_entries", "grinqh_vmm_lut",
     "grinqh_vmm_lut_threshold", "grinqh_set_option", "grinqh_calibrate_noalloc",
-    "grinqh_last_error",
+    "grinqh_stream_read", "grinqh_last_error",
 )
 
 
@@ -90,6 +90,7 @@ def _load():
         "grinqh_vmm_lut_threshold": [dp, vp, vp, vp, i32, ctypes.POINTER(ctypes.c_float), vp, vp, i32, vp],
         "grinqh_set_option": [ctypes.c_int, ctypes.c_int],
         "grinqh_calibrate_noalloc": [dp, vp, i32, ctypes.POINTER(i32), vp, vp],
+        "grinqh_stream_read": [vp, sz, vp, vp],
     }
     for name, args in sig.items():
         f = getattr(lib, name)
@@ -414,3 +415,11 @@ def grinqh_vmm_lut_threshold(desc: LayerDesc, packed_codes, luts, x, thresholds,
     _check(lib.grinqh_vmm_lut_threshold(ctypes.byref(rd), cp, lp, xp, B, _thresholds(rd, thresholds), lo, yp,
                                         flags, _stream(stream)))
     return y
+
+
+def grinqh_stream_read(src, sink, stream=None):
+    """Stream-read the uint8 device tensor src (measurement infrastructure)."""
+    torch = _torch()
+    sp = _dev(src, torch.uint8, "src")
+    kp = _dev(sink, torch.int32, "sink", (1,))
+    _check(lib.grinqh_stream_read(sp, src.numel(), kp, _stream(stream)))
