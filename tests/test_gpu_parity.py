@@ -185,6 +185,7 @@ def test_vmm_topk_parity(g, torch, K, N, levels, tile_n, B):
     for p in inputs.BUDGETS[tuple(levels)].values():
         counts = g.grinqh_topk_counts(K, p)
         lm = _host(g.grinqh_assign(L.desc, _dev(torch, x), g.GRINQH_ASSIGN_TOPK, counts=counts))
+        assert np.array_equal(lm, orc.assign_topk(x, counts)), p
         y, ref = _vmm_case(g, torch, L, x, lm)
         assert normwise(y, ref) <= TOL, (p, normwise(y, ref))
 
@@ -363,6 +364,115 @@ def test_full_size_pack_and_sampled_vmm(g, torch, name, K, N, levels, xkind):
     y4 = _host(g.grinqh_vmm(L.desc, L.pc, L.ps, _dev(torch, x4), lm4))
     ref4 = orc.vmm_batch(L.codes[rows], L.scales[:, rows], x4, _host(lm4), levels)
     assert normwise(y4[:, rows], ref4) <= TOL, (name, "B=4")
+
+
+def oracle_all_outputs(codes, scales, x, lm, levels, chunk=2048):
+    """The float64 oracle over every output, a block of outputs at a time
+    (the dense float64 weights of a 4096 x 28672 layer would take 0.9 GB)."""
+    N = codes.shape[0]
+    return np.concatenate([orc.vmm_batch(codes[n:n + chunk], scales[:, n:n + chunk], x, lm, levels)
+                           for n in range(0, N, chunk)], axis=1)
+
+
+def elementwise(y, ref):
+    """Largest |y_n - ref_n| / max(|ref_n|, 1e-2 max|ref|) (reported, not gated)."""
+    y, ref = np.asarray(y, dtype=np.float64), np.asarray(ref, dtype=np.float64)
+    den = np.maximum(np.abs(ref), 1e-2 * np.abs(ref).max(axis=-1, keepdims=True))
+    return float((np.abs(y - ref) / den).max())
+
+
+# every output of one full-size shape per kernel instance the benchmarks run
+EVERY = [
+    ("batch1 T=256 k 4096->1024", 4096, 1024, inputs.LEVELS_B, "t3", 1),
+    ("batch1 T=512 qkv 4096->6144", 4096, 6144, inputs.LEVELS_B, "t3", 1),
+    ("batch1 T=1024 gate|up 4096->28672", 4096, 28672, inputs.LEVELS_B, "t3", 1),
+    ("batch1 T=1024 down 14336->4096", 14336, 4096, inputs.LEVELS_B, "swiglu", 1),
+    ("per-plane B=2 qkv 4096->6144", 4096, 6144, inputs.LEVELS_B, "t3", 2),
+    ("per-plane B=4 down 14336->4096", 14336, 4096, inputs.LEVELS_B, "swiglu", 4),
+    ("1-bit planes qkv 4096->6144", 4096, 6144, inputs.LEVELS_C, "t3", 1),
+]
+
+
+@pytest.mark.parametrize("name,K,N,levels,xkind,B", EVERY, ids=[e[0] for e in EVERY])
+def test_full_size_every_output(g, torch, name, K, N, levels, xkind, B):
+    # thresholds calibrated on separate tokens (the runtime path), grading
+    # fused into the VMM, level maps written out and checked bit for bit
+    L = Layer(g, torch, K, N, levels, cfg=75, layer=K + N, codes_src=True)
+    gen = inputs.activations_swiglu if xkind == "swiglu" else inputs.activations_t3
+    x = gen(K, B, 75, K + N)
+    calib = gen(K, 64, 76, K + N)
+    budget = 4 if 4 in inputs.BUDGETS[tuple(levels)] else 3
+    th = _host(g.grinqh_calibrate(L.desc, _dev(torch, calib), inputs.BUDGETS[tuple(levels)][budget]))
+    lm_out = torch.zeros((B, K), dtype=torch.uint8, device="cuda")
+    y = _host(g.grinqh_vmm_threshold(L.desc, L.pc, L.ps, _dev(torch, x), th, level_map_out=lm_out))
+    lm = orc.assign_threshold(x, th)
+    assert np.array_equal(_host(lm_out), lm)
+    ref = oracle_all_outputs(L.codes, L.scales, x, lm, levels)
+    err = normwise(y, ref)
+    print(f"{name}: normwise {err:.2e}, elementwise {elementwise(y, ref):.2e}")
+    assert err <= TOL, (name, err)
+
+
+def test_decode_layers_graph_replays_match_oracle(g, torch):
+    # Two layers of the decode step (merged q|k|v, o, merged gate|up, down at
+    # 4 bits, thresholds calibrated per input, grading fused) captured as one
+    # HIP graph with the output buffer cleared inside it, replayed three times
+    # with eager work and synchronisation between; every replay checked
+    # against the oracle on every output of every linear.
+    levels = inputs.LEVELS_B
+    shapes = [("qkv", 4096, 6144, 0, "t3"), ("o", 4096, 4096, 1, "t3"),
+              ("gate_up", 4096, 28672, 2, "t3"), ("down", 14336, 4096, 3, "swiglu")]
+    layers = [{name: Layer(g, torch, K, N, levels, cfg=77, layer=10 * li + xin, codes_src=True)
+               for name, K, N, xin, _ in shapes} for li in range(2)]
+    xs, ths = {}, {}
+    p = inputs.BUDGETS[levels][4]
+    for name, K, N, xin, kind in shapes:
+        gen = inputs.activations_swiglu if kind == "swiglu" else inputs.activations_t3
+        xs[xin] = gen(K, 1, 77, xin)
+        ths[xin] = _host(g.grinqh_calibrate(layers[0][name].desc, _dev(torch, gen(K, 32, 78, xin)), p))
+    xd = {k: _dev(torch, v) for k, v in xs.items()}
+    width = sum(N for _, _, N, _, _ in shapes)
+    arena = torch.zeros(2 * width, dtype=torch.float32, device="cuda")
+    outs, off = [], 0
+    for li in range(2):
+        per = {}
+        for name, _, N, _, _ in shapes:
+            per[name] = arena[off:off + N].view(1, N)
+            off += N
+        outs.append(per)
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+
+    def step():
+        arena.zero_()
+        for li in range(2):
+            for name, _, _, xin, _ in shapes:
+                Ly = layers[li][name]
+                g.grinqh_vmm_threshold(Ly.desc, Ly.pc, Ly.ps, xd[xin], ths[xin], y=outs[li][name],
+                                       accumulate=True)
+
+    with torch.cuda.stream(s):
+        step()
+    torch.cuda.synchronize()
+    refs = {}
+    for li in range(2):
+        for name, _, _, xin, _ in shapes:
+            Ly = layers[li][name]
+            lm = orc.assign_threshold(xs[xin], ths[xin])
+            refs[li, name] = oracle_all_outputs(Ly.codes, Ly.scales, xs[xin], lm, levels)
+    gr = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(gr, stream=s):
+        step()
+    for rep in range(3):
+        arena.fill_(float("nan"))              # eager work between replays
+        torch.cuda.synchronize()
+        with torch.cuda.stream(s):
+            gr.replay()
+        torch.cuda.synchronize()
+        for li in range(2):
+            for name, _, _, _, _ in shapes:
+                err = normwise(_host(outs[li][name]), refs[li, name])
+                assert err <= TOL, (rep, li, name, err)
 
 
 @pytest.mark.parametrize("kernel", ["pp", "dot2"])
