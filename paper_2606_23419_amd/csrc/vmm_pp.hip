@@ -6,23 +6,28 @@
 // them, with two ballots, into "big" rows (3 or 4 planes to read) and "small"
 // rows (1 or 2).  A batch gives each lane group either two big rows, planes
 // 1-4 of each, or four small rows, planes 1-2 of each: eight plane dwords per
-// lane either way, consumed as two merged plane pairs.  The plane a row may
-// lack (plane 4 of a 3-plane row, plane 2 of a 1-plane row) is read from an
-// offset outside the tile's buffer resource, which returns zero without a
-// memory access; a zero plane is exactly what truncating the code to the
-// row's depth leaves there.  So every batch issues the same loads and runs
-// the same dequant, with no branch on the kind of batch.
+// lane either way.  The plane a row may lack (plane 4 of a 3-plane row,
+// plane 2 of a 1-plane row) is read from an offset outside the tile's buffer
+// resource, which returns zero without a memory access; a zero plane is
+// exactly what truncating the code to the row's depth leaves there.  Every
+// batch issues the same loads; a group's big batches come first, so the kind
+// of a batch is one scalar compare.
 //
-// A plane pair (j, j+1) of two channels: the two 2-bit fields of an output
-// merge into one 4-bit field F = 4 c_j + c_(j+1) worth F 2^(6-2j); v_perm_b32
-// puts one byte of each channel in the two halves of a dword, v_and_or_b32
-// adds the exponent bits E = 31 - 2j - p (fp16 bias 15) so the field at bit p
-// reads as 2^(16-2j-p) + F 2^(6-2j), and one v_dot2_f32_f16 with (x_k1, x_k2)
-// adds both channels.  The offsets the exponent bits add are summed per lane
-// alongside and taken out at the end of each group:
-//   y_n += s_{g,n} (acc_n - f(n) off + beta_g),
+// Small batches: a plane pair (j, j+1) of two channels.  The two 2-bit fields
+// of an output merge into one 4-bit field F = 4 c_j + c_(j+1) worth
+// F 2^(6-2j); v_perm_b32 puts one byte of each channel in the two halves of a
+// dword, v_and_or_b32 adds the exponent bits E = 31 - 2j - p (fp16 bias 15)
+// so the field at bit p reads as 2^(16-2j-p) + F 2^(6-2j), and one
+// v_dot2_f32_f16 with (x_k1, x_k2) adds both channels.  The offsets the
+// exponent bits add are summed per lane alongside and taken out at the end
+// of each group:
+//   y_n += s_{g,n} (acc_n - f(n) off - off8 + beta_g),
 // with f = 2^(-p) for the output's field position p and beta_g = sum over the
 // wave's active rows of x_k (phi_b - 128) (midpoint bias and code offset).
+//
+// Big batches: the four planes of two channels merge into each output's full
+// 8-bit code, read with exponent bits 25 as 2^10 + F, one v_dot2_f32_f16 per
+// output for both channels; their offset 2^10 per channel is summed in off8.
 // The waves meet once, to sum their partial outputs.
 #include "grinqh_internal.h"
 #include "vmm_common.h"
@@ -54,6 +59,44 @@ __device__ __forceinline__ void consume_double(uint32_t w1a, uint32_t w1b, uint3
       acc[e + 2] = dot2r((lo & 0x00F000F0u) | m4, xp, acc[e + 2]);
       acc[e + 4] = dot2r((hi & 0x000F000Fu) | m0, xp, acc[e + 4]);
       acc[e + 6] = dot2r((hi & 0x00F000F0u) | m4, xp, acc[e + 6]);
+    }
+  }
+}
+
+// Planes 1-4 of 16 outputs, two channels (a = first row, b = second): the
+// four 2-bit fields of an output merge into its full 8-bit code
+// F = 64 c_1 + 16 c_2 + 4 c_3 + c_4, which with exponent bits 25 reads as
+// 2^10 + F in fp16, so one v_dot2_f32_f16 adds both channels' codes.  The
+// nibble pairs (1,2) and (3,4) are merged first as in consume_double, then
+// a byte takes the pair-(1,2) nibble on top of the pair-(3,4) nibble; output
+// e keeps the accumulator it has in consume_double.
+__device__ __forceinline__ void consume_quad(const uint32_t (&w)[8], uint32_t xp,
+                                             float (&acc)[16]) {
+  constexpr uint32_t kHi = 0xCCCCCCCCu, kLo = 0x33333333u, kNib = 0x0F0F0F0Fu;
+  constexpr uint32_t kExp = 0x64006400u;   // exponent bits 25 in both halves
+  uint32_t X[2][4];   // [channel][L_E, L_O, H_E, H_O]
+#pragma unroll
+  for (int c = 0; c < 2; ++c) {
+    const uint32_t p1 = w[2 * c], p2 = w[2 * c + 1], p3 = w[4 + 2 * c], p4 = w[5 + 2 * c];
+    const uint32_t E12 = ((p1 << 2) & kHi) | (p2 & kLo), O12 = (p1 & kHi) | ((p2 >> 2) & kLo);
+    const uint32_t E34 = ((p3 << 2) & kHi) | (p4 & kLo), O34 = (p3 & kHi) | ((p4 >> 2) & kLo);
+    X[c][0] = ((E12 << 4) & ~kNib) | (E34 & kNib);   // low nibbles of E bytes
+    X[c][1] = ((O12 << 4) & ~kNib) | (O34 & kNib);
+    X[c][2] = (E12 & ~kNib) | ((E34 >> 4) & kNib);   // high nibbles of E bytes
+    X[c][3] = (O12 & ~kNib) | ((O34 >> 4) & kNib);
+  }
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int s = q & 1, n = q >> 1;   // E/O set, nibble of the byte
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      // bytes 2h and 2h+1 of both channels: [a_k, b_k, a_k+1, b_k+1]
+      const uint32_t G = __builtin_amdgcn_perm(X[1][q], X[0][q], h ? 0x07030602u : 0x05010400u);
+      const uint32_t lo = __builtin_amdgcn_perm(kExp, G, 0x07010500u);
+      const uint32_t hi = __builtin_amdgcn_perm(kExp, G, 0x07030502u);
+      const int e = s + 2 * n + 8 * h;
+      acc[e] = dot2r(lo, xp, acc[e]);
+      acc[e + 4] = dot2r(hi, xp, acc[e + 4]);
     }
   }
 }
@@ -159,10 +202,12 @@ __global__ __launch_bounds__(256) void k_vmm_sr(
     }
   }
   const int nb_v = valid ? nbb + nsb : 0;
+  const int nbb_v = valid ? nbb : 0;
   int nb_g[MAXG];
   float beta_g[MAXG];
   nb_g[0] = __builtin_amdgcn_readlane(nb_v, 0);
   nb_g[1] = __builtin_amdgcn_readlane(nb_v, 32);
+  const int nbb0 = __builtin_amdgcn_readlane(nbb_v, 0), nbb1 = __builtin_amdgcn_readlane(nbb_v, 32);
   beta_g[0] = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, bs), 0));
   beta_g[1] = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, bs), 32));
   // the lists and the empty batch are this wave's own: its LDS accesses
@@ -174,7 +219,7 @@ __global__ __launch_bounds__(256) void k_vmm_sr(
 
   // ---- main loop over this wave's (group, batch) sequence: D register sets,
   // D-1 batches in flight while one is consumed
-  float yp[16], acc[16], off = 0.0f;
+  float yp[16], acc[16], off = 0.0f, off8 = 0.0f;
 #pragma unroll
   for (int e = 0; e < 16; ++e) yp[e] = acc[e] = 0.0f;
 
@@ -203,6 +248,11 @@ __global__ __launch_bounds__(256) void k_vmm_sr(
     B.w[6] = load_plane(rsrc, o1.w + li4);
     B.w[7] = load_plane(rsrc, o2.w + li4);
   };
+  auto consume_big = [&](const Batch& B) {
+    const uint32_t xp = __builtin_amdgcn_perm(B.xe[1], B.xe[0], 0x05040100u);
+    off8 = dot2r(0x64006400u, xp, off8);
+    consume_quad(B.w, xp, acc);
+  };
   auto consume = [&](const Batch& B) {
     // (x_k1, x_k2) from the entries' low halves, the exponent bits from the high halves
     const uint32_t xpa = __builtin_amdgcn_perm(B.xe[1], B.xe[0], 0x05040100u);
@@ -214,26 +264,34 @@ __global__ __launch_bounds__(256) void k_vmm_sr(
     consume_double(B.w[0], B.w[1], B.w[2], B.w[3], m0a, xpa, acc);
     consume_double(B.w[4], B.w[5], B.w[6], B.w[7], m0b, xpb, acc);
   };
-  auto finish_group = [&](int g) {
+  // the group being consumed, the end of its big batches and of all its
+  // batches (a group without batches has no rows to add and is skipped)
+  int cur_g = nb_g[0] > 0 ? 0 : 1;
+  int cur_bigend = cur_g == 0 ? nbb0 : bstart1 + nbb1;
+  int next_fin = cur_g == 0 ? bstart1 : nbt;
+  auto finish_group = [&]() {
     float sc[16];
-    const uint32_t ww[8] = {scw[g][0].x, scw[g][0].y, scw[g][0].z, scw[g][0].w,
-                            scw[g][1].x, scw[g][1].y, scw[g][1].z, scw[g][1].w};
+    const bool g1 = cur_g != 0;
+    const uint32_t ww[8] = {g1 ? scw[1][0].x : scw[0][0].x, g1 ? scw[1][0].y : scw[0][0].y,
+                            g1 ? scw[1][0].z : scw[0][0].z, g1 ? scw[1][0].w : scw[0][0].w,
+                            g1 ? scw[1][1].x : scw[0][1].x, g1 ? scw[1][1].y : scw[0][1].y,
+                            g1 ? scw[1][1].z : scw[0][1].z, g1 ? scw[1][1].w : scw[0][1].w};
 #pragma unroll
     for (int h = 0; h < 8; ++h) {
       sc[2 * h] = h2f((uint16_t)(ww[h] & 0xFFFFu));
       sc[2 * h + 1] = h2f((uint16_t)(ww[h] >> 16));
     }
-    const float beta = lg == 0 ? beta_g[g] : 0.0f;
+    const float beta = lg == 0 ? (g1 ? beta_g[1] : beta_g[0]) : 0.0f;
 #pragma unroll
     for (int e = 0; e < 16; ++e) {
-      yp[e] = fmaf(sc[e], acc[e] - double_offset_factor(e) * off + beta, yp[e]);
+      yp[e] = fmaf(sc[e], acc[e] - double_offset_factor(e) * off - off8 + beta, yp[e]);
       acc[e] = 0.0f;
     }
     off = 0.0f;
-  };
-  auto after = [&](int b) {
-    if (b + 1 == bstart1) finish_group(0);
-    if (b + 1 == nbt) finish_group(1);
+    off8 = 0.0f;
+    cur_g = 1;
+    cur_bigend = bstart1 + nbb1;
+    next_fin = nbt;
   };
 
   // the first batches in order (a scheduler free to reorder them issues
@@ -248,11 +306,13 @@ __global__ __launch_bounds__(256) void k_vmm_sr(
 #pragma unroll
     for (int i = 0; i < D; ++i) {
       fetch(R[(i + D - 1) % D], b + i + D - 1);
+      __builtin_amdgcn_sched_barrier(0);   // the loads go out before the consume waits
       // a guard, not an exit: an early exit out of the unrolled body makes
       // the loop header wait for every load in flight
       if (b + i < nbt) {
-        consume(R[i]);
-        after(b + i);
+        if (b + i < cur_bigend) consume_big(R[i]);
+        else consume(R[i]);
+        if (b + i + 1 == next_fin) finish_group();
       }
     }
   }
