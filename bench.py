@@ -543,7 +543,7 @@ def run_decode(args, torch, g):
         "algorithmic_bytes_per_vmm": round(main["step_bytes"] / n_vmm, 1),
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
-                     "kernel": "k_vmm_sr (every VMM launch of the step), HIP events over a graph of them",
+                     "kernel": "k_vmm_sr / k_vmm_sg (every VMM launch of the step), HIP events over a graph of them",
                      **({"measured_read_ceiling": ceiling,
                          "frac_of_measured_ceiling": round(achieved / ceiling, 4)} if ceiling else {})},
         "per_layer": per_layer,

@@ -333,14 +333,285 @@ __global__ __launch_bounds__(256) void k_vmm_sr(
   }
 }
 
+// The same VMM with the lists of a workgroup shared: the four waves' rows of
+// a group form one list (big rows, then small, in wave order) and the waves
+// take its batches in turn (wave w: batches w, w + 4, ...).  That evens the
+// waves' work and pads each list once per group rather than once per wave,
+// for two workgroup barriers in the prologue; it pays on launches of two
+// groups per workgroup, where each wave otherwise pads four lists.
+template <int LPR, int D>
+__global__ __launch_bounds__(256) void k_vmm_sg(
+    const uint8_t* __restrict__ codes, const uint16_t* __restrict__ scales,
+    const uint16_t* __restrict__ x, const uint8_t* __restrict__ lm, float* __restrict__ y,
+    Layer L, int gw, int fused, Thresholds th, uint8_t* __restrict__ lm_out) {
+  constexpr int T = LPR * 16;            // outputs of the tile
+  constexpr int PLANE = T / 4;           // bytes of one plane row
+  constexpr int NLG = 64 / LPR;          // lane groups per wave
+  constexpr int kWaves = 4;
+  constexpr int MAXG = 2;                // groups per workgroup at most; gw is 1 or 2
+  constexpr int BR = 2 * NLG;            // big rows per batch
+  constexpr int SR = 4 * NLG;            // small rows per batch
+  constexpr int MB = kGroup / BR + 2;   // batches of one group's list at most
+  constexpr int EMPTY = MAXG * MB;       // an all-empty batch after the lists
+  constexpr int ENT = NLG * 12;          // dwords of one batch
+  // fp16 exponent bits of a merged pair's field at p = 0: 31 - 2j for the
+  // pair of planes (j, j+1); 27 for empty entries (any finite value)
+  constexpr uint32_t kE12 = 29u << 10, kE34 = 25u << 10, kEmpty = 27u << 10;
+
+  // lists: per batch and lane group four entries as three 4-dword fields:
+  // offsets of plane j, of plane j+1, and (x | exponent << 16); a list's
+  // batches lie back to back, group 0's then group 1's
+  __shared__ __align__(16) uint32_t s_ent[EMPTY + 1][NLG][12];
+  __shared__ __align__(16) float s_red[kWaves][T];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int half = lane >> 5, hl = lane & 31;
+  const int t = blockIdx.x % L.tiles;
+  const int g0 = (blockIdx.x / L.tiles) * gw;
+  const int ng = min(gw, L.groups - g0);
+  const int lg = lane / LPR, li = lane % LPR;
+  const int n_top = L.n_levels - 1;
+  const __amdgpu_buffer_rsrc_t rsrc = tile_rsrc(codes + (size_t)t * L.K * L.RB, L);
+  const uint32_t li4 = (uint32_t)li * 4u;
+
+  // ---- loads first: x and the level map of this lane's row (lanes 0-31 the
+  // first group, 32-63 the second), the scales of this lane's 16 outputs for
+  // both groups (a group past the last reads the last one again, from cache)
+  const int gg = half;
+  const bool valid = gg < ng;
+  const int k = (g0 + min(gg, ng - 1)) * kGroup + 32 * wave + hl;
+  const uint32_t xv = x[k];
+  const uint32_t lv = (fused ? (const uint8_t*)x : lm)[k];   // ignored in fused mode
+  uint4 scw[MAXG][2];
+#pragma unroll
+  for (int g = 0; g < MAXG; ++g) {
+    const uint16_t* sp = scales + (size_t)(g0 + min(g, ng - 1)) * L.N + (size_t)t * T + li * 16;
+    scw[g][0] = *(const uint4*)sp;
+    scw[g][1] = *(const uint4*)(sp + 8);
+  }
+  uint32_t* const E = &s_ent[0][0][0];
+  if (wave == 0 && lane < ENT) E[EMPTY * ENT + lane] = (lane % 12) < 8 ? kNoRow : (kEmpty << 16);
+
+  // ---- grade, sort into big and small rows
+  const float fx = h2f((uint16_t)xv);
+  const float ax = fabsf(fx);
+  int graded = 0;
+#pragma unroll
+  for (int j = 0; j < kMaxLevels - 1; ++j) graded += ax >= th.theta[j] ? 1 : 0;
+  const int lvl = min(fused ? graded : (int)(lv & 0xFFu), n_top);
+  if (fused && lm_out && t == 0 && valid) lm_out[k] = (uint8_t)lvl;
+  const int d = valid ? level_planes(L.planes_packed, lvl) : 0;
+  const bool big = d >= 3, small = d == 1 || d == 2;
+  const int nbig = half_total(big), nsm = half_total(small);   // this half wave's rows
+  const int rank = big ? half_below(big) : half_below(small);
+  const float bs = half_sum_dpp(d ? fx * phi_minus_offset(2 * d, L.bmax) : 0.0f);
+
+  // rows of each group's list, and those of this lane's list before this wave's
+  int NB[MAXG], NS[MAXG];
+  int below_big = 0, below_sm = 0;
+  {
+    __shared__ int s_cnt[kWaves][MAXG][2];
+    if (hl == 0) {
+      s_cnt[wave][gg][0] = nbig;
+      s_cnt[wave][gg][1] = nsm;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int g = 0; g < MAXG; ++g) {
+      NB[g] = NS[g] = 0;
+#pragma unroll
+      for (int w = 0; w < kWaves; ++w) {
+        const int cb = s_cnt[w][g][0], cs = s_cnt[w][g][1];
+        if (w < wave && g == gg) {
+          below_big += cb;
+          below_sm += cs;
+        }
+        NB[g] += cb;
+        NS[g] += cs;
+      }
+    }
+  }
+  const int nbb0 = (NB[0] + BR - 1) / BR, nsb0 = (NS[0] + SR - 1) / SR;
+  const int nbb1 = (NB[1] + BR - 1) / BR, nsb1 = (NS[1] + SR - 1) / SR;
+  const int bstart1 = nbb0 + nsb0;
+  const int nbt = bstart1 + nbb1 + nsb1;
+
+  // ---- write the lists
+  {
+    const uint32_t base = (uint32_t)k * (uint32_t)L.RB;
+    const uint32_t xh = xv & 0xFFFFu;
+    const int st = gg ? bstart1 : 0, nbb_gg = gg ? nbb1 : nbb0, nsb_gg = gg ? nsb1 : nsb0;
+    auto put = [&](int b, int lgp, int sl, uint32_t o1, uint32_t o2, uint32_t xe) {
+      uint32_t* p = E + b * ENT + lgp * 12 + sl;
+      p[0] = o1;
+      p[4] = o2;
+      p[8] = xe;
+    };
+    if (valid && big) {
+      const int r = below_big + rank;
+      const int b = st + r / BR, w = r % BR;
+      put(b, w >> 1, w & 1, base, base + PLANE, xh | (kE12 << 16));
+      put(b, w >> 1, (w & 1) + 2, base + 2 * PLANE, d >= 4 ? base + 3 * PLANE : kNoRow,
+          xh | (kE34 << 16));
+    }
+    if (valid && small) {
+      const int r = below_sm + rank;
+      const int b = st + nbb_gg + r / SR, w = r % SR;
+      put(b, w >> 2, w & 3, base, d >= 2 ? base + PLANE : kNoRow, xh | (kE12 << 16));
+    }
+    // empty entries up to whole batches (no memory access, zero
+    // coefficient), by the last wave's half of each group
+    if (valid && wave == kWaves - 1) {
+      const int nb_end = gg ? NB[1] : NB[0], ns_end = gg ? NS[1] : NS[0];
+      for (int r = nb_end + hl; r < nbb_gg * BR; r += 32) {
+        const int b = st + r / BR, w = r % BR;
+        put(b, w >> 1, w & 1, kNoRow, kNoRow, kEmpty << 16);
+        put(b, w >> 1, (w & 1) + 2, kNoRow, kNoRow, kEmpty << 16);
+      }
+      for (int r = ns_end + hl; r < nsb_gg * SR; r += 32) {
+        const int b = st + nbb_gg + r / SR, w = r % SR;
+        put(b, w >> 2, w & 3, kNoRow, kNoRow, kEmpty << 16);
+      }
+    }
+  }
+  float beta_g[MAXG];   // this wave's rows: it adds them with its partial sums
+  beta_g[0] = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, bs), 0));
+  beta_g[1] = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, bs), 32));
+  __syncthreads();
+
+  // ---- main loop over this wave's batches of the sequence (group 0 big,
+  // small, group 1 big, small): D register sets, D-1 batches in flight while
+  // one is consumed
+  float yp[16], acc[16], off = 0.0f, off8 = 0.0f;
+#pragma unroll
+  for (int e = 0; e < 16; ++e) yp[e] = acc[e] = 0.0f;
+
+  struct Batch {
+    uint32_t w[8];
+    uint32_t xe[4];
+  };
+  const uint32_t lane_ent = (uint32_t)lg * 12u;
+  auto fetch = [&](Batch& B, int q) {
+    const int idx = q < nbt ? q : EMPTY;
+    const uint32_t* src = E + idx * ENT + lane_ent;
+    const uint4 o1 = *(const uint4*)src;
+    const uint4 o2 = *(const uint4*)(src + 4);
+    const uint4 xe = *(const uint4*)(src + 8);
+    B.xe[0] = xe.x;
+    B.xe[1] = xe.y;
+    B.xe[2] = xe.z;
+    B.xe[3] = xe.w;
+    B.w[0] = load_plane(rsrc, o1.x + li4);
+    B.w[1] = load_plane(rsrc, o2.x + li4);
+    B.w[2] = load_plane(rsrc, o1.y + li4);
+    B.w[3] = load_plane(rsrc, o2.y + li4);
+    B.w[4] = load_plane(rsrc, o1.z + li4);
+    B.w[5] = load_plane(rsrc, o2.z + li4);
+    B.w[6] = load_plane(rsrc, o1.w + li4);
+    B.w[7] = load_plane(rsrc, o2.w + li4);
+  };
+  auto consume_big = [&](const Batch& B) {
+    const uint32_t xp = __builtin_amdgcn_perm(B.xe[1], B.xe[0], 0x05040100u);
+    off8 = dot2r(0x64006400u, xp, off8);
+    consume_quad(B.w, xp, acc);
+  };
+  auto consume = [&](const Batch& B) {
+    // (x_k1, x_k2) from the entries' low halves, the exponent bits from the high halves
+    const uint32_t xpa = __builtin_amdgcn_perm(B.xe[1], B.xe[0], 0x05040100u);
+    const uint32_t m0a = __builtin_amdgcn_perm(B.xe[1], B.xe[0], 0x07060302u);
+    const uint32_t xpb = __builtin_amdgcn_perm(B.xe[3], B.xe[2], 0x05040100u);
+    const uint32_t m0b = __builtin_amdgcn_perm(B.xe[3], B.xe[2], 0x07060302u);
+    off = dot2r(m0a, xpa, off);
+    off = dot2r(m0b, xpb, off);
+    consume_double(B.w[0], B.w[1], B.w[2], B.w[3], m0a, xpa, acc);
+    consume_double(B.w[4], B.w[5], B.w[6], B.w[7], m0b, xpb, acc);
+  };
+  // the group being consumed and the end of its big batches; every wave
+  // finishes both groups (a group it has no batch of adds its rows' beta)
+  int cur_g = 0;
+  int cur_bigend = nbb0;
+  auto finish_group = [&]() {
+    float sc[16];
+    const bool g1 = cur_g != 0;
+    const uint32_t ww[8] = {g1 ? scw[1][0].x : scw[0][0].x, g1 ? scw[1][0].y : scw[0][0].y,
+                            g1 ? scw[1][0].z : scw[0][0].z, g1 ? scw[1][0].w : scw[0][0].w,
+                            g1 ? scw[1][1].x : scw[0][1].x, g1 ? scw[1][1].y : scw[0][1].y,
+                            g1 ? scw[1][1].z : scw[0][1].z, g1 ? scw[1][1].w : scw[0][1].w};
+#pragma unroll
+    for (int h = 0; h < 8; ++h) {
+      sc[2 * h] = h2f((uint16_t)(ww[h] & 0xFFFFu));
+      sc[2 * h + 1] = h2f((uint16_t)(ww[h] >> 16));
+    }
+    const float beta = lg == 0 ? (g1 ? beta_g[1] : beta_g[0]) : 0.0f;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      yp[e] = fmaf(sc[e], acc[e] - double_offset_factor(e) * off - off8 + beta, yp[e]);
+      acc[e] = 0.0f;
+    }
+    off = 0.0f;
+    off8 = 0.0f;
+    cur_g = 1;
+    cur_bigend = bstart1 + nbb1;
+  };
+  constexpr int kStride = kWaves;
+  const int first = wave;
+  const int nbw = nbt > first ? (nbt - first + kStride - 1) / kStride : 0;   // this wave's batches
+  if (first >= bstart1) finish_group();   // no batch of group 0 for this wave
+
+  // the first batches in order (a scheduler free to reorder them issues
+  // batch 0 last, and its consume then waits for all of them)
+  Batch R[D];
+#pragma unroll
+  for (int i = 0; i < D - 1; ++i) {
+    fetch(R[i], first + kStride * i);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  for (int b = 0; b < nbw; b += D) {
+#pragma unroll
+    for (int i = 0; i < D; ++i) {
+      fetch(R[(i + D - 1) % D], first + kStride * (b + i + D - 1));
+      __builtin_amdgcn_sched_barrier(0);   // the loads go out before the consume waits
+      // a guard, not an exit: an early exit out of the unrolled body makes
+      // the loop header wait for every load in flight
+      if (b + i < nbw) {
+        const int q = first + kStride * (b + i);
+        if (q < cur_bigend) consume_big(R[i]);
+        else consume(R[i]);
+        if (cur_g == 0 && q + kStride >= bstart1) finish_group();
+      }
+    }
+  }
+  finish_group();   // group 1 (a group past the last adds zero)
+
+  // ---- reduce: lane groups of a wave by lane swaps, waves through LDS, then
+  // one atomic add per output
+#pragma unroll
+  for (int e = 0; e < 16; ++e) yp[e] = lane_group_sum<LPR>(yp[e]);
+  if (lane < LPR) {
+#pragma unroll
+    for (int c = 0; c < 4; ++c)
+      *(float4*)&s_red[wave][li * 16 + 4 * c] = make_float4(yp[4 * c], yp[4 * c + 1], yp[4 * c + 2], yp[4 * c + 3]);
+  }
+  __syncthreads();
+  for (int o = tid; o < T; o += 256) {
+    const float v = s_red[0][o] + s_red[1][o] + s_red[2][o] + s_red[3][o];
+    atomicAdd(&y[(size_t)t * T + o], v * L.sfac);   // 8-bit code units -> b_max units
+  }
+}
+
 template <int LPR>
 void launch_sr(int gw, hipStream_t s, const void* codes, const void* scales, const void* x,
                const uint8_t* lm, float* y, const Layer& L, int fused, const Thresholds& th,
                uint8_t* lm_out) {
   const dim3 grid((unsigned)(L.tiles * ((L.groups + gw - 1) / gw)));
-  hipLaunchKernelGGL((k_vmm_sr<LPR, 4>), grid, dim3(256), 0, s,
-                     (const uint8_t*)codes, (const uint16_t*)scales, (const uint16_t*)x, lm, y, L,
-                     gw, fused, th, lm_out);
+  if (gw == 2)
+    hipLaunchKernelGGL((k_vmm_sg<LPR, 4>), grid, dim3(256), 0, s,
+                       (const uint8_t*)codes, (const uint16_t*)scales, (const uint16_t*)x, lm, y, L,
+                       gw, fused, th, lm_out);
+  else
+    hipLaunchKernelGGL((k_vmm_sr<LPR, 4>), grid, dim3(256), 0, s,
+                       (const uint8_t*)codes, (const uint16_t*)scales, (const uint16_t*)x, lm, y, L,
+                       gw, fused, th, lm_out);
 }
 
 }  // namespace
