@@ -81,7 +81,7 @@ __global__ __launch_bounds__(kThreadsPF) void k_prefill(const uint8_t* __restric
                                                        const uint16_t* __restrict__ scales,
                                                        const uint16_t* __restrict__ x,
                                                        float* __restrict__ y, Layer L, int M,
-                                                       int accumulate) {
+                                                       int accumulate, int2 win) {
   constexpr int BM = 64 * MB, BN = 64 * NB;
   constexpr int XI = BM * kBK * 2 / 1024 / 4;      // X copy instructions per wave and step
   constexpr int WI = kBK * BN / 1024 / 4;          // code copy instructions per wave and step
@@ -101,7 +101,23 @@ __global__ __launch_bounds__(kThreadsPF) void k_prefill(const uint8_t* __restric
   __shared__ __align__(16) uint8_t sP1[kBK * BN];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int m0 = blockIdx.x * BM, n0 = blockIdx.y * BN;
+  // Workgroup i runs on XCD i mod 8.  The (row block, column tile) pairs are
+  // taken in windows of win.x row blocks by win.y column tiles, and each XCD
+  // gets a contiguous run of that order: the workgroups an XCD runs together
+  // share their X rows and weight columns in its L2 (win.x = 1 when the
+  // grid does not split into windows: row blocks in order).
+  int rblk, ctile;
+  {
+    const int gx = (M + BM - 1) / BM;
+    const int G = (int)gridDim.x, i = (int)blockIdx.x;
+    const int xcd = i & 7, j = i >> 3, per = G >> 3, extra = G & 7;
+    const int pos = xcd * per + min(xcd, extra) + j;
+    const int wsz = win.x * win.y, w = pos / wsz, p = pos - w * wsz;
+    const int wr = w % (gx / win.x), wc = w / (gx / win.x);
+    rblk = win.x * wr + p / win.y;
+    ctile = win.y * wc + p % win.y;
+  }
+  const int m0 = rblk * BM, n0 = ctile * BN;
   const int T = L.T, K = L.K, N = L.N;
   const int steps = K / kBK;                       // even: K is a multiple of 128
   const int tile = n0 / T, o0 = n0 - tile * T;     // BN divides T
@@ -308,9 +324,16 @@ __global__ __launch_bounds__(kThreadsPF) void k_prefill(const uint8_t* __restric
 template <int U, int MB, int NB>
 void launch_cfg(const Layer& L, const void* codes, const void* scales, const void* x, int M,
                 float* y, int accumulate, hipStream_t s) {
-  const dim3 grid((unsigned)((M + 64 * MB - 1) / (64 * MB)), (unsigned)(L.N / (64 * NB)));
-  hipLaunchKernelGGL((k_prefill<U, MB, NB>), grid, dim3(kThreadsPF), 0, s, (const uint8_t*)codes,
-                     (const uint16_t*)scales, (const uint16_t*)x, y, L, M, accumulate);
+  const int gx = (M + 64 * MB - 1) / (64 * MB), gy = L.N / (64 * NB);
+  // windows of up to 4 row blocks x 8 column tiles (about one XCD's worth of
+  // workgroups at one per CU), the largest powers of two dividing the grid
+  int2 win = make_int2(1, 1);
+  while (win.x < 4 && gx % (2 * win.x) == 0) win.x *= 2;
+  while (win.y < 8 && gy % (2 * win.y) == 0) win.y *= 2;
+  if (win.x == 1) win.y = 1;   // one row block: the plain order already shares X
+  hipLaunchKernelGGL((k_prefill<U, MB, NB>), dim3((unsigned)(gx * gy)), dim3(kThreadsPF), 0, s,
+                     (const uint8_t*)codes, (const uint16_t*)scales, (const uint16_t*)x, y, L, M,
+                     accumulate, win);
 }
 
 template <int U>
