@@ -7,8 +7,9 @@
 // x_k * table_b[n][q_b].
 //
 // A workgroup owns 64 outputs of one tile (a sub-tile), a run of groups and
-// one token.  The tables of its 64 outputs, every level, are copied to LDS
-// once: for each level they are one contiguous block of the table array.
+// one token.  It stages the run's levels and x, and copies to LDS the tables
+// of its 64 outputs for the levels the run uses: for each level they are one
+// contiguous block of the table array.
 // 4 lanes cover a channel row's 64 outputs (16 each); the 64 row slots of
 // the workgroup take two rows of each group.  Every weight is one LDS
 // lookup.  Lanes holding the same outputs are reduced with shuffles, waves
@@ -45,6 +46,7 @@ __global__ __launch_bounds__(kLutThreads) void k_vmm_lut(const uint8_t* __restri
   __shared__ int s_cum[kMaxLevels];                           // level l's block starts at s_cum[l]
   __shared__ uint8_t s_lv[kMaxRun];                           // levels of the run's channels
   __shared__ uint16_t s_x[kMaxRun];                           // x of the run's channels
+  __shared__ uint32_t s_used;                                 // bit l: level l has a channel
 
   // Work order: the K splits of a sub-tile, then the sub-tiles of a tile,
   // are consecutive work items, and consecutive items run on one XCD
@@ -70,31 +72,6 @@ __global__ __launch_bounds__(kLutThreads) void k_vmm_lut(const uint8_t* __restri
   // starts are 128-byte multiples apart, the same banks for every b >= 2)
   const int pad = D.quad_pad;
   if (tid < kMaxLevels) s_cum[tid] = kSub * D.cum[tid] + 4 * pad * max(tid - 1, 0);
-  // tables of the 64 outputs: level l's are kSub * 2^b entries at
-  // D.offset[l] + n0 * 2^b of the table array, 8 * 2^b pieces of 16 bytes,
-  // copied quad by quad.  A thread issues eight loads before its eight
-  // stores: one L2 latency per eight pieces rather than one per piece.
-  for (int l = 1; l < L.n_levels; ++l) {
-    const int b = L.bits[l];
-    const int np = 8 << b, qn = 2 << b;      // pieces of the level, of a quad
-    const uint4* src = (const uint4*)(luts + D.offset[l] + ((size_t)n0 << b));
-    uint16_t* dst = s_lut + kSub * D.cum[l] + 4 * pad * (l - 1);
-    for (int i0 = 0; i0 < np; i0 += 8 * kLutThreads) {
-      uint4 v[8];
-#pragma unroll
-      for (int q = 0; q < 8; ++q) v[q] = src[min(i0 + tid + q * kLutThreads, np - 1)];
-      __builtin_amdgcn_sched_barrier(0);     // keep the eight loads ahead of the stores
-#pragma unroll
-      for (int q = 0; q < 8; ++q) {
-        // (past the last piece: the last piece again, the same value to the
-        // same place, so that neither loads nor stores are conditional)
-        const int i = min(i0 + tid + q * kLutThreads, np - 1);
-        *(uint4*)(dst + (i / qn) * ((16 << b) + pad) + 8 * (i % qn)) = v[q];
-      }
-    }
-  }
-  __syncthreads();
-
   const int c = tid & 3;                     // outputs 16 c .. 16 c + 15 of the sub-tile
   const int rs = tid >> 2;                   // row slot: rows rs, rs + 64, ... of the run
   const int plane_bytes = L.T * U / 8;
@@ -102,6 +79,9 @@ __global__ __launch_bounds__(kLutThreads) void k_vmm_lut(const uint8_t* __restri
   const int n_top = L.n_levels - 1;
   const int kr0 = g0 * kGroup, nrows = (g1 - g0) * kGroup;   // the workgroup's channels
 
+  uint32_t used = 0;
+  if (tid == 0) s_used = 0;
+  __syncthreads();
   // levels and x of the run's channels, staged once (<= kMaxRun channels):
   // read from the level map, or graded here from |x| against the thresholds
   // (Sec. 3.1; th.n is 0 without them), the level map then written out once
@@ -123,8 +103,19 @@ __global__ __launch_bounds__(kLutThreads) void k_vmm_lut(const uint8_t* __restri
     }
     s_lv[i] = (uint8_t)lv;
     s_x[i] = xh;
+    used |= 1u << lv;
+  }
+  // the levels any channel of the run uses: only their tables are copied
+  // (at the paper's 4-bit budgets the 8-bit level, three quarters of the
+  // table bytes, is empty)
+  {
+    uint32_t u = used;
+#pragma unroll
+    for (int m = 1; m < 64; m <<= 1) u |= (uint32_t)__shfl_xor((int)u, m);
+    if (lane == 0) atomicOr(&s_used, u);
   }
   __syncthreads();
+  const uint32_t used_levels = s_used;
 
   float acc[16];
 #pragma unroll
@@ -186,6 +177,33 @@ __global__ __launch_bounds__(kLutThreads) void k_vmm_lut(const uint8_t* __restri
   uint32_t wr[R][kWords];
 #pragma unroll
   for (int q = 0; q < R - 1; ++q) fetch(rs + 64 * q, wr[q]);
+  __builtin_amdgcn_sched_barrier(0);   // the first rows' loads go out before the table copy
+  // tables of the 64 outputs: level l's are kSub * 2^b entries at
+  // D.offset[l] + n0 * 2^b of the table array, 8 * 2^b pieces of 16 bytes,
+  // copied quad by quad.  A thread issues eight loads before its eight
+  // stores: one L2 latency per eight pieces rather than one per piece.
+  for (int l = 1; l < L.n_levels; ++l) {
+    if (!((used_levels >> l) & 1u)) continue;
+    const int b = L.bits[l];
+    const int np = 8 << b, qn = 2 << b;      // pieces of the level, of a quad
+    const uint4* src = (const uint4*)(luts + D.offset[l] + ((size_t)n0 << b));
+    uint16_t* dst = s_lut + kSub * D.cum[l] + 4 * pad * (l - 1);
+    for (int i0 = 0; i0 < np; i0 += 8 * kLutThreads) {
+      uint4 v[8];
+#pragma unroll
+      for (int q = 0; q < 8; ++q) v[q] = src[min(i0 + tid + q * kLutThreads, np - 1)];
+      __builtin_amdgcn_sched_barrier(0);     // keep the eight loads ahead of the stores
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        // (past the last piece: the last piece again, the same value to the
+        // same place, so that neither loads nor stores are conditional)
+        const int i = min(i0 + tid + q * kLutThreads, np - 1);
+        *(uint4*)(dst + (i / qn) * ((16 << b) + pad) + 8 * (i % qn)) = v[q];
+      }
+    }
+  }
+  __syncthreads();
+
   for (int i = rs; i < nrows; i += 64 * R) {
 #pragma unroll
     for (int q = 0; q < R; ++q) {
