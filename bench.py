@@ -11,7 +11,10 @@ Assignment modes (--assign):
              separate set of calibration tokens (grinqh_calibrate), grading
              fused into the VMM.  Per token: one VMM launch per projection.
   topk       the exact-budget form: a top-k assignment launch per distinct
-             input, then the VMMs.
+             input, then the VMMs.  At batch 1 the line also times the same
+             step with the selection fused into each VMM launch
+             (grinqh_vmm_topk, `topk_fused`), which measures slower: every
+             workgroup repeats the whole selection.
 The default is threshold; the JSON line also carries the top-k step.
 
 One step is the whole hot path for every token, captured once as a HIP graph
@@ -338,6 +341,24 @@ def buf_bytes_gbs(nbytes, ms):
     return nbytes / (ms * 1e-3) / 1e9
 
 
+def fused_topk_layers(g, torch, descs, weights, xs, counts, layers):
+    """The layers the batch-1 VMM with top-k selection fused in takes (2-bit
+    planes, tiles of 256, 512 or 1024 outputs), found by one eager call each."""
+    ok = {}
+    for name, _, N, xin, _ in layers:
+        y = torch.zeros((1, N), dtype=torch.float32, device=xs[xin].device)
+        try:
+            g.grinqh_vmm_topk(descs[name], weights[name][0], weights[name][1], xs[xin][:1],
+                              counts[xin], y=y)
+            ok[name] = True
+        except g.GrinqhError as e:
+            if e.status != g.GRINQH_EUNSUPPORTED:
+                raise
+            ok[name] = False
+    torch.cuda.synchronize()
+    return ok
+
+
 def run_decode(args, torch, g):
     """The full decode step: n_layers x (qkv, o, gate_up, down) at batch B.
 
@@ -383,6 +404,7 @@ def run_decode(args, torch, g):
 
     thresholds = thresholds_for(p_bp)
     counts = {xin: g.grinqh_topk_counts(int(xs[xin].shape[1]), p_bp) for xin in xs}
+    fused_topk = B == 1 and all(fused_topk_layers(g, torch, descs, weights[0], xs, counts, layers).values())
     lm = {xin: torch.zeros((B, int(x.shape[1])), dtype=torch.uint8, device=dev) for xin, x in xs.items()}
     # The step's outputs live in one buffer, cleared once per step (one fill
     # launch), and every VMM accumulates into its own zeroed slice: a decoder
@@ -411,6 +433,10 @@ def run_decode(args, torch, g):
                     g.grinqh_vmm_threshold(descs[name], w[name][0], w[name][1], xs[xin], th[xin],
                                            y=out[li][name], level_map_out=lm[xin] if li == 0 else None,
                                            accumulate=True)
+                elif mode == "topk_fused":
+                    g.grinqh_vmm_topk(descs[name], w[name][0], w[name][1], xs[xin], counts[xin],
+                                      y=out[li][name], level_map_out=lm[xin] if li == 0 else None,
+                                      accumulate=True)
                 else:
                     g.grinqh_assign(descs[name], xs[xin], g.GRINQH_ASSIGN_TOPK, counts=counts[xin],
                                     out=lm[xin])
@@ -455,7 +481,11 @@ def run_decode(args, torch, g):
                        for _, K, N, xin, _ in layers)
 
     out_modes = {}
-    for mode in (args.assign, "topk" if args.assign == "threshold" else "threshold"):
+    modes = [args.assign, "topk" if args.assign == "threshold" else "threshold"] + (["topk_fused"] if fused_topk else [])
+    for mode in modes:
+        if mode == "topk_fused":
+            for m in lm.values():
+                m.fill_(255)
         with torch.cuda.stream(s):
             step(mode, thresholds)
         torch.cuda.synchronize()
@@ -479,6 +509,9 @@ def run_decode(args, torch, g):
                            "achieved_avg_bits": {f"input{xin}": round(float(np.asarray(levels)[m].mean()), 4)
                                                  for xin, m in lm_host.items()},
                            "lm_host": lm_host, "per_rep": per_rep}
+        if mode == "topk_fused" and not all(np.array_equal(lm_host[xin], out_modes["topk"]["lm_host"][xin])
+                                            for xin in lm_host):
+            raise RuntimeError("the fused top-k level maps differ from the top-k assignment's")
         del gr
     main = out_modes[args.assign]
     other = "topk" if args.assign == "threshold" else "threshold"
@@ -550,6 +583,8 @@ def run_decode(args, torch, g):
         **({"vs_bits": vs_bits} if vs_bits else {}),
         "other_assignment": dict(assignment=other, **{k: v for k, v in out_modes[other].items()
                                                        if k not in ("step_bytes", "lm_host", "per_rep")}),
+        **({"topk_fused": {k: v for k, v in out_modes["topk_fused"].items()
+                           if k in ("ms_per_step", "value")}} if "topk_fused" in out_modes else {}),
     }
     if not args.no_cpu and B == 1:
         res["cpu_baseline"] = cpu_baseline_decode(wl, {xin: t for xin, t in thresholds.items()},

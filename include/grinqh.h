@@ -200,6 +200,21 @@ GRINQH_API int grinqh_vmm_threshold(const grinqh_layer_desc* desc, const void* p
                          const float* thresholds, uint8_t* level_map_out, float* y,
                          int32_t flags, void* workspace, size_t ws_bytes, void* stream);
 
+/* The batch-1 VMM with the exact top-k assignment of App. A.1 fused into
+ * it: every workgroup selects the token's per-level cuts from the whole x
+ * (the counts[j] channels of largest |x| at level j from the top, ties to the
+ * lower channel index, exactly as grinqh_assign in top-k mode) and grades its
+ * own channels against them, so no level map is read and no assignment
+ * launch is needed.  counts: int32 [n_levels] (host), summing to K.
+ * Requires B = 1, K <= 16384, 2-bit planes with tile_n in {256, 512, 1024}
+ * (GRINQH_EUNSUPPORTED otherwise: grinqh_assign + grinqh_vmm serve the
+ * other cases) and x 16-byte aligned.  level_map_out, if not NULL, receives
+ * the levels (uint8 [K]).  Other arguments as grinqh_vmm. */
+GRINQH_API int grinqh_vmm_topk(const grinqh_layer_desc* desc, const void* packed_codes,
+                               const void* packed_scales, const void* x, int32_t B,
+                               const int32_t* counts, uint8_t* level_map_out, float* y,
+                               int32_t flags, void* workspace, size_t ws_bytes, void* stream);
+
 /* Prefill, the stage-decoupled dense path (Sec. 3: prefill reads the weights
  * at the fixed top precision; Sec. 4 "Prefill vs. Decoding Evaluation"): for
  * M tokens at once, every channel at all b_max bits,

@@ -238,6 +238,26 @@ int grinqh_calibrate_noalloc(const grinqh_layer_desc* desc, const void* x, int32
   return launch_calibrate_noalloc(L, x, S, qp, theta, (hipStream_t)stream);
 }
 
+// Per-level channel counts -> cumulative cuts C_j (channels at level >= j + 1).
+static int topk_cuts(const Layer& L, const int32_t* counts, TopkCuts* cuts) {
+  if (!counts) return fail(GRINQH_EINVAL, "counts is NULL");
+  if (L.K > 16384) return fail(GRINQH_EUNSUPPORTED, "top-k assignment needs K <= 16384 (K=%d)", L.K);
+  long long total = 0;
+  for (int j = 0; j < L.n_levels; ++j) {
+    if (counts[j] < 0) return fail(GRINQH_EINVAL, "counts[%d]=%d is negative", j, counts[j]);
+    total += counts[j];
+  }
+  if (total != L.K) return fail(GRINQH_EINVAL, "counts sum to %lld, not K=%d", total, L.K);
+  cuts->n = L.n_levels - 1;
+  for (int j = 0; j < kMaxLevels; ++j) {
+    long long c = 0;
+    if (j < cuts->n)
+      for (int i = j + 1; i < L.n_levels; ++i) c += counts[i];
+    cuts->cum[j] = (int)c;
+  }
+  return GRINQH_OK;
+}
+
 int grinqh_assign(const grinqh_layer_desc* desc, int mode, const void* x, int32_t B,
                   const float* thresholds, const int32_t* counts, uint8_t* level_map,
                   void* workspace, size_t ws_bytes, void* stream) {
@@ -257,22 +277,9 @@ int grinqh_assign(const grinqh_layer_desc* desc, int mode, const void* x, int32_
   }
   if (mode == GRINQH_ASSIGN_TOPK) {
     if (thresholds) return fail(GRINQH_EINVAL, "thresholds must be NULL in top-k mode");
-    if (!counts) return fail(GRINQH_EINVAL, "counts is NULL");
-    if (L.K > 16384) return fail(GRINQH_EUNSUPPORTED, "top-k assignment needs K <= 16384 (K=%d)", L.K);
-    long long total = 0;
-    for (int j = 0; j < L.n_levels; ++j) {
-      if (counts[j] < 0) return fail(GRINQH_EINVAL, "counts[%d]=%d is negative", j, counts[j]);
-      total += counts[j];
-    }
-    if (total != L.K) return fail(GRINQH_EINVAL, "counts sum to %lld, not K=%d", total, L.K);
     TopkCuts cuts;
-    cuts.n = L.n_levels - 1;
-    for (int j = 0; j < kMaxLevels; ++j) {
-      long long c = 0;
-      if (j < cuts.n)
-        for (int i = j + 1; i < L.n_levels; ++i) c += counts[i];
-      cuts.cum[j] = (int)c;
-    }
+    st = topk_cuts(L, counts, &cuts);
+    if (st) return st;
     return launch_assign_topk(L, x, B, cuts, level_map, (hipStream_t)stream);
   }
   return fail(GRINQH_EINVAL, "mode=%d is not a known assignment mode", mode);
@@ -320,9 +327,31 @@ int grinqh_vmm_threshold(const grinqh_layer_desc* desc, const void* packed_codes
   Thresholds th;
   st = check_thresholds(L, thresholds, &th);
   if (st) return st;
-  if ((uintptr_t)level_map_out & 1u) return fail(GRINQH_EINVAL, "level_map_out must be 2-byte aligned");
   return launch_vmm(L, packed_codes, packed_scales, x, nullptr, &th, level_map_out, B, y,
                     flags & GRINQH_VMM_ACCUMULATE, (hipStream_t)stream);
+}
+
+int grinqh_vmm_topk(const grinqh_layer_desc* desc, const void* packed_codes,
+                    const void* packed_scales, const void* x, int32_t B, const int32_t* counts,
+                    uint8_t* level_map_out, float* y, int32_t flags, void* workspace,
+                    size_t ws_bytes, void* stream) {
+  clear_error();
+  (void)workspace; (void)ws_bytes;
+  Layer L;
+  int st = resolve(desc, &L, nullptr);
+  if (st) return st;
+  st = vmm_common_checks(L, packed_codes, packed_scales, x, B, y, flags);
+  if (st) return st;
+  TopkCuts cuts;
+  st = topk_cuts(L, counts, &cuts);
+  if (st) return st;
+  if (B != 1 || !vmm_pp_supported(L, 1) || option(&Options::vmm_kernel))
+    return fail(GRINQH_EUNSUPPORTED,
+                "the fused top-k VMM runs at B = 1 on 2-bit planes with T in {256, 512, 1024}; "
+                "use grinqh_assign (top-k) and grinqh_vmm");
+  if (((uintptr_t)x & 15u)) return fail(GRINQH_EINVAL, "x must be 16-byte aligned in top-k mode");
+  return launch_vmm_topk(L, packed_codes, packed_scales, x, cuts, level_map_out, y,
+                         flags & GRINQH_VMM_ACCUMULATE, (hipStream_t)stream);
 }
 
 int grinqh_prefill(const grinqh_layer_desc* desc, const void* packed_codes,

@@ -100,9 +100,15 @@ constexpr int kCalibScratch = 1 << 17;   // 1 MiB
 int launch_calibrate_noalloc(const Layer& L, const void* x, int S, const QuantilePos& qp,
                              float* theta, hipStream_t s);
 bool vmm_pp_supported(const Layer& L, int B);
+// levels from the level map, or graded in the kernel from thresholds (th) or
+// the exact top-k cuts of x (tk), then optionally written to level_map_out
 int launch_vmm_pp(const Layer& L, const void* codes, const void* scales, const void* x,
-                  const uint8_t* level_map, const Thresholds* th, uint8_t* level_map_out,
-                  float* y, hipStream_t s);
+                  const uint8_t* level_map, const Thresholds* th, const TopkCuts* tk,
+                  uint8_t* level_map_out, float* y, hipStream_t s);
+// the batch-1 VMM with exact top-k assignment in its prologue (B = 1)
+int launch_vmm_topk(const Layer& L, const void* codes, const void* scales, const void* x,
+                    const TopkCuts& cuts, uint8_t* level_map_out, float* y, int accumulate,
+                    hipStream_t s);
 bool vmm_dot2_supported(const Layer& L);
 int launch_vmm_dot2(const Layer& L, const void* codes, const void* scales, const void* x,
                     const uint8_t* level_map, const Thresholds* th, uint8_t* level_map_out,

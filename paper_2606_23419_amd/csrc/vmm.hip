@@ -156,7 +156,7 @@ int launch_vmm(const Layer& L, const void* codes, const void* scales, const void
   const int force = option(&Options::vmm_kernel);   // tests and measurements
   const bool want_dot2 = force == GRINQH_KERNEL_PER_PLANE, want_v0 = force == GRINQH_KERNEL_GENERAL;
   if (!want_dot2 && !want_v0 && vmm_pp_supported(L, B))
-    return launch_vmm_pp(L, codes, scales, x, level_map, th, level_map_out, y, s);
+    return launch_vmm_pp(L, codes, scales, x, level_map, th, nullptr, level_map_out, y, s);
   if (!want_v0 && vmm_dot2_supported(L))
     return launch_vmm_dot2(L, codes, scales, x, level_map, th, level_map_out, B, y, s);
   // about 512 workgroups per token over the whole chip
@@ -176,6 +176,17 @@ int launch_vmm(const Layer& L, const void* codes, const void* scales, const void
                        (const uint16_t*)scales, (const uint16_t*)x, level_map, y, L, gps, fused,
                        fused ? *th : none, level_map_out);
   return check_launch("vmm");
+}
+
+int launch_vmm_topk(const Layer& L, const void* codes, const void* scales, const void* x,
+                    const TopkCuts& cuts, uint8_t* level_map_out, float* y, int accumulate,
+                    hipStream_t s) {
+  if (!accumulate) {
+    hipLaunchKernelGGL(k_zero, dim3((unsigned)((L.N + 255) / 256)), dim3(256), 0, s, y, (long)L.N);
+    int st = check_launch("vmm zero-fill");
+    if (st) return st;
+  }
+  return launch_vmm_pp(L, codes, scales, x, nullptr, nullptr, &cuts, level_map_out, y, s);
 }
 
 }  // namespace grinqh

@@ -30,6 +30,7 @@
 // output for both channels; their offset 2^10 per channel is summed in off8.
 // The waves meet once, to sum their partial outputs.
 #include "grinqh_internal.h"
+#include "topk_select.h"
 #include "vmm_common.h"
 
 namespace grinqh {
@@ -109,7 +110,7 @@ template <int LPR, int D>
 __global__ __launch_bounds__(256) void k_vmm_sr(
     const uint8_t* __restrict__ codes, const uint16_t* __restrict__ scales,
     const uint16_t* __restrict__ x, const uint8_t* __restrict__ lm, float* __restrict__ y,
-    Layer L, int gw, int fused, Thresholds th, uint8_t* __restrict__ lm_out) {
+    Layer L, int gw, int fused, Thresholds th, TopkCuts tk, uint8_t* __restrict__ lm_out) {
   constexpr int T = LPR * 16;            // outputs of the tile
   constexpr int PLANE = T / 4;           // bytes of one plane row
   constexpr int NLG = 64 / LPR;          // lane groups per wave
@@ -145,7 +146,7 @@ __global__ __launch_bounds__(256) void k_vmm_sr(
   const bool valid = gg < ng;
   const int k = (g0 + min(gg, ng - 1)) * kGroup + 32 * wave + hl;
   const uint32_t xv = x[k];
-  const uint32_t lv = (fused ? (const uint8_t*)x : lm)[k];   // ignored in fused mode
+  const uint32_t lv = (fused ? (const uint8_t*)x : lm)[k];   // ignored when graded here
   uint4 scw[MAXG][2];
 #pragma unroll
   for (int g = 0; g < MAXG; ++g) {
@@ -155,13 +156,20 @@ __global__ __launch_bounds__(256) void k_vmm_sr(
   }
   if (lane < 12) (&s_empty[wave][0][0])[lane] = lane < 8 ? kNoRow : (kEmpty << 16);
 
+  // top-k mode: the token's cuts from the whole x, the same in every workgroup
+  __shared__ __align__(16) topksel::Scratch s_tk;
+  if (fused == 2) topksel::select_cuts(x, L.K, tk, s_tk);
+
   // ---- grade, sort into big and small rows, write this wave's lists
   const float fx = h2f((uint16_t)xv);
   const float ax = fabsf(fx);
   int graded = 0;
 #pragma unroll
   for (int j = 0; j < kMaxLevels - 1; ++j) graded += ax >= th.theta[j] ? 1 : 0;
-  const int lvl = min(fused ? graded : (int)(lv & 0xFFu), n_top);
+  const int lvl = min(fused == 1 ? graded
+                      : fused == 2 ? topksel::level_of(xv, k, tk.n, s_tk)
+                                   : (int)(lv & 0xFFu),
+                      n_top);
   if (fused && lm_out && t == 0 && valid) lm_out[k] = (uint8_t)lvl;
   const int d = valid ? level_planes(L.planes_packed, lvl) : 0;
   const bool big = d >= 3, small = d == 1 || d == 2;
@@ -343,7 +351,7 @@ template <int LPR, int D>
 __global__ __launch_bounds__(256) void k_vmm_sg(
     const uint8_t* __restrict__ codes, const uint16_t* __restrict__ scales,
     const uint16_t* __restrict__ x, const uint8_t* __restrict__ lm, float* __restrict__ y,
-    Layer L, int gw, int fused, Thresholds th, uint8_t* __restrict__ lm_out) {
+    Layer L, int gw, int fused, Thresholds th, TopkCuts tk, uint8_t* __restrict__ lm_out) {
   constexpr int T = LPR * 16;            // outputs of the tile
   constexpr int PLANE = T / 4;           // bytes of one plane row
   constexpr int NLG = 64 / LPR;          // lane groups per wave
@@ -381,7 +389,7 @@ __global__ __launch_bounds__(256) void k_vmm_sg(
   const bool valid = gg < ng;
   const int k = (g0 + min(gg, ng - 1)) * kGroup + 32 * wave + hl;
   const uint32_t xv = x[k];
-  const uint32_t lv = (fused ? (const uint8_t*)x : lm)[k];   // ignored in fused mode
+  const uint32_t lv = (fused ? (const uint8_t*)x : lm)[k];   // ignored when graded here
   uint4 scw[MAXG][2];
 #pragma unroll
   for (int g = 0; g < MAXG; ++g) {
@@ -392,13 +400,20 @@ __global__ __launch_bounds__(256) void k_vmm_sg(
   uint32_t* const E = &s_ent[0][0][0];
   if (wave == 0 && lane < ENT) E[EMPTY * ENT + lane] = (lane % 12) < 8 ? kNoRow : (kEmpty << 16);
 
+  // top-k mode: the token's cuts from the whole x, the same in every workgroup
+  __shared__ __align__(16) topksel::Scratch s_tk;
+  if (fused == 2) topksel::select_cuts(x, L.K, tk, s_tk);
+
   // ---- grade, sort into big and small rows
   const float fx = h2f((uint16_t)xv);
   const float ax = fabsf(fx);
   int graded = 0;
 #pragma unroll
   for (int j = 0; j < kMaxLevels - 1; ++j) graded += ax >= th.theta[j] ? 1 : 0;
-  const int lvl = min(fused ? graded : (int)(lv & 0xFFu), n_top);
+  const int lvl = min(fused == 1 ? graded
+                      : fused == 2 ? topksel::level_of(xv, k, tk.n, s_tk)
+                                   : (int)(lv & 0xFFu),
+                      n_top);
   if (fused && lm_out && t == 0 && valid) lm_out[k] = (uint8_t)lvl;
   const int d = valid ? level_planes(L.planes_packed, lvl) : 0;
   const bool big = d >= 3, small = d == 1 || d == 2;
@@ -602,16 +617,16 @@ __global__ __launch_bounds__(256) void k_vmm_sg(
 template <int LPR>
 void launch_sr(int gw, hipStream_t s, const void* codes, const void* scales, const void* x,
                const uint8_t* lm, float* y, const Layer& L, int fused, const Thresholds& th,
-               uint8_t* lm_out) {
+               const TopkCuts& tk, uint8_t* lm_out) {
   const dim3 grid((unsigned)(L.tiles * ((L.groups + gw - 1) / gw)));
   if (gw == 2)
     hipLaunchKernelGGL((k_vmm_sg<LPR, 4>), grid, dim3(256), 0, s,
                        (const uint8_t*)codes, (const uint16_t*)scales, (const uint16_t*)x, lm, y, L,
-                       gw, fused, th, lm_out);
+                       gw, fused, th, tk, lm_out);
   else
     hipLaunchKernelGGL((k_vmm_sr<LPR, 4>), grid, dim3(256), 0, s,
                        (const uint8_t*)codes, (const uint16_t*)scales, (const uint16_t*)x, lm, y, L,
-                       gw, fused, th, lm_out);
+                       gw, fused, th, tk, lm_out);
 }
 
 }  // namespace
@@ -623,19 +638,21 @@ bool vmm_pp_supported(const Layer& L, int B) {
 }
 
 int launch_vmm_pp(const Layer& L, const void* codes, const void* scales, const void* x,
-                  const uint8_t* level_map, const Thresholds* th, uint8_t* level_map_out,
-                  float* y, hipStream_t s) {
+                  const uint8_t* level_map, const Thresholds* th, const TopkCuts* tk,
+                  uint8_t* level_map_out, float* y, hipStream_t s) {
   // groups per workgroup: about 512 workgroups, rounded to the nearest count
   // (896 (tile, group) units -> 2, 448 -> 1)
   int gw = (int)(((long)L.tiles * L.groups + 256) / 512);
   if (const int v = option(&Options::groups_per_wg)) gw = v;
   gw = gw < 1 ? 1 : (gw > 2 ? 2 : gw);
   Thresholds none{};
+  TopkCuts nocuts{};
   const Thresholds& tt = th ? *th : none;
-  const int fused = th != nullptr;
-  if (L.T == 256) launch_sr<16>(gw, s, codes, scales, x, level_map, y, L, fused, tt, level_map_out);
-  else if (L.T == 512) launch_sr<32>(gw, s, codes, scales, x, level_map, y, L, fused, tt, level_map_out);
-  else launch_sr<64>(gw, s, codes, scales, x, level_map, y, L, fused, tt, level_map_out);
+  const TopkCuts& cc = tk ? *tk : nocuts;
+  const int fused = th ? 1 : (tk ? 2 : 0);   // levels graded here: thresholds, top-k
+  if (L.T == 256) launch_sr<16>(gw, s, codes, scales, x, level_map, y, L, fused, tt, cc, level_map_out);
+  else if (L.T == 512) launch_sr<32>(gw, s, codes, scales, x, level_map, y, L, fused, tt, cc, level_map_out);
+  else launch_sr<64>(gw, s, codes, scales, x, level_map, y, L, fused, tt, cc, level_map_out);
   return check_launch("vmm (sorted rows)");
 }
 

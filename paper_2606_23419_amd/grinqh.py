@@ -39,7 +39,7 @@ EXPORTED = (
     "grinqh_workspace_bytes", "grinqh_calibrate", "grinqh_assign", "grinqh_vmm",
     "grinqh_vmm_threshold", "grinqh_prefill", "grinqh_lut_entries", "grinqh_vmm_lut",
     "grinqh_vmm_lut_threshold", "grinqh_set_option", "grinqh_calibrate_noalloc",
-    "grinqh_stream_read", "grinqh_last_error",
+    "grinqh_stream_read", "grinqh_vmm_topk", "grinqh_last_error",
 )
 
 
@@ -91,6 +91,7 @@ def _load():
         "grinqh_set_option": [ctypes.c_int, ctypes.c_int],
         "grinqh_calibrate_noalloc": [dp, vp, i32, ctypes.POINTER(i32), vp, vp],
         "grinqh_stream_read": [vp, sz, vp, vp],
+        "grinqh_vmm_topk": [dp, vp, vp, vp, i32, ctypes.POINTER(i32), vp, vp, i32, vp, sz, vp],
     }
     for name, args in sig.items():
         f = getattr(lib, name)
@@ -331,6 +332,30 @@ def grinqh_vmm_threshold(desc: LayerDesc, packed_codes, packed_scales, x, thresh
     flags = _vmm_flags(accumulate)
     _check(lib.grinqh_vmm_threshold(ctypes.byref(rd), cp, sp, xp, B, _thresholds(rd, thresholds), lo,
                                     yp, flags, None, 0, _stream(stream)))
+    return y
+
+
+def grinqh_vmm_topk(desc: LayerDesc, packed_codes, packed_scales, x, counts, y=None,
+                    level_map_out=None, accumulate: bool = False, stream=None):
+    """The batch-1 VMM with exact top-k assignment fused in (counts per level,
+    summing to K); optionally writes the level map."""
+    torch = _torch()
+    rd = grinqh_resolve_desc(desc)
+    if x.dim() == 1:
+        x = x.view(1, -1)
+    B = int(x.shape[0])
+    cp = _dev(packed_codes, torch.uint8, "packed_codes", (rd.K * rd.N * rd.level_bits[rd.n_levels - 1] // 8,))
+    sp = _dev(packed_scales, torch.float16, "packed_scales", (rd.K // 128, rd.N))
+    xp = _dev(x, torch.float16, "x", (B, rd.K))
+    cn = _host_array([int(c) for c in counts], rd.n_levels, ctypes.c_int32, "counts")
+    lo = _dev(level_map_out, torch.uint8, "level_map_out", (B, rd.K)) \
+        if level_map_out is not None else None
+    if y is None:
+        y = torch.empty((B, rd.N), dtype=torch.float32, device=x.device)
+    yp = _dev(y, torch.float32, "y", (B, rd.N))
+    flags = _vmm_flags(accumulate)
+    _check(lib.grinqh_vmm_topk(ctypes.byref(rd), cp, sp, xp, B, cn, lo, yp, flags, None, 0,
+                               _stream(stream)))
     return y
 
 

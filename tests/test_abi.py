@@ -199,6 +199,25 @@ def test_vmm_validation(g):
     assert g.grinqh_last_error()
 
 
+def test_vmm_topk_validation(g):
+    d = g.make_desc(256, 512, (0, 2, 4, 8), tile_n=512)
+    V = g.lib.grinqh_vmm_topk
+    cn = _cn([64, 64, 64, 64])
+    assert V(ctypes.byref(d), FAKE, FAKE, FAKE, 1, None, None, FAKE, 0, None, 0, None) == -1
+    assert V(ctypes.byref(d), FAKE, FAKE, FAKE, 1, _cn([64, 64, 64, 63]), None, FAKE, 0, None, 0, None) == -1
+    assert V(ctypes.byref(d), FAKE, FAKE, FAKE, 1, _cn([-1, 65, 128, 64]), None, FAKE, 0, None, 0, None) == -1
+    assert V(ctypes.byref(d), FAKE, FAKE, FAKE, 1, cn, None, FAKE, 4, None, 0, None) == -1
+    assert V(ctypes.byref(d), FAKE, FAKE, ctypes.c_void_p(0x1008), 1, cn, None, FAKE, 0, None, 0, None) == -1
+    assert "16-byte" in g.grinqh_last_error()
+    assert V(ctypes.byref(d), FAKE, FAKE, FAKE, 2, cn, None, FAKE, 0, None, 0, None) == -2   # batch 1 only
+    odd = g.make_desc(256, 512, (0, 2, 3, 4, 8), tile_n=512)                              # 1-bit planes
+    assert V(ctypes.byref(odd), FAKE, FAKE, FAKE, 1, _cn([64, 64, 64, 32, 32]), None, FAKE, 0, None, 0,
+             None) == -2
+    big = g.make_desc(128 * 129, 512, (0, 8), tile_n=512)
+    assert V(ctypes.byref(big), FAKE, FAKE, FAKE, 1, _cn([0, 128 * 129]), None, FAKE, 0, None, 0, None) == -2
+    assert "K <= 16384" in g.grinqh_last_error()
+
+
 def test_prefill_validation(g):
     d = g.make_desc(256, 512, (0, 2, 4, 8))
     P = g.lib.grinqh_prefill

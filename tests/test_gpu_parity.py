@@ -271,6 +271,88 @@ def test_vmm_threshold_fused(g, torch, levels):
     assert normwise(_host(y), ref) <= TOL
 
 
+def _topk_fused_case(g, torch, L, x, counts, accumulate_check=False):
+    """Fused top-k VMM against the oracle (level map bit-exact, y normwise) and
+    against the two-launch path (assign, then VMM)."""
+    K = L.K
+    lm_out = torch.full((1, K), 255, dtype=torch.uint8, device="cuda")
+    xd = _dev(torch, x)
+    y = g.grinqh_vmm_topk(L.desc, L.pc, L.ps, xd, counts, level_map_out=lm_out)
+    lm2 = g.grinqh_assign(L.desc, xd, g.GRINQH_ASSIGN_TOPK, counts=counts)
+    y2 = g.grinqh_vmm(L.desc, L.pc, L.ps, xd, lm2)
+    torch.cuda.synchronize()
+    lm = orc.assign_topk(x, counts)
+    assert np.array_equal(_host(lm_out), lm), counts
+    # same kernel and level map; the groups' partial sums meet in atomics, so
+    # the two agree to float32 rounding of the order of additions
+    assert normwise(_host(y), _host(y2)) <= 1e-6, counts
+    ref = orc.vmm_batch(L.codes, L.scales, x, lm, L.levels)
+    assert normwise(_host(y), ref) <= TOL, (counts, normwise(_host(y), ref))
+    if accumulate_check:
+        y0 = torch.from_numpy(np.full((1, L.N), 0.75, np.float32)).cuda()
+        g.grinqh_vmm_topk(L.desc, L.pc, L.ps, xd, counts, y=y0, accumulate=True)
+        torch.cuda.synchronize()
+        assert normwise(_host(y0) - 0.75, ref) <= TOL
+
+
+@pytest.mark.parametrize("K,N,levels,tile_n", [
+    (128, 512, (0, 2, 4, 8), 512), (640, 1024, (0, 2, 4, 6, 8), 256), (1152, 2048, (0, 2, 4, 8), 1024),
+    (4096, 4096, (0, 2, 4, 6, 8), 512), (4096, 1024, (0, 2, 4, 6), 256), (2048, 2048, (0, 2, 4), 512),
+    (14336, 1024, (0, 2, 4, 6, 8), 1024), (16384, 512, (0, 2, 4, 8), 512)])
+def test_vmm_topk_fused(g, torch, K, N, levels, tile_n):
+    L = Layer(g, torch, K, N, levels, cfg=64, tile_n=tile_n)
+    x = (inputs.activations_swiglu if K >= 4096 else inputs.activations_t3)(K, 1, 64)
+    for i, p in enumerate(inputs.BUDGETS[tuple(levels)].values()):
+        _topk_fused_case(g, torch, L, x, g.grinqh_topk_counts(K, p), accumulate_check=i == 0)
+
+
+@pytest.mark.parametrize("case", ["ties", "all_equal", "zeros", "signed_zero", "extreme_counts"])
+def test_vmm_topk_fused_adversarial(g, torch, case):
+    K, N = 1024, 1024
+    L = Layer(g, torch, K, N, (0, 2, 4, 8), cfg=65, tile_n=512)
+    rng = np.random.default_rng(65)
+    if case == "ties":
+        x = rng.choice(np.array([0.5, -0.5, 1.0, 2.0, -2.0, 0.0], np.float16), size=(1, K))
+    elif case == "all_equal":
+        x = np.full((1, K), -1.25, dtype=np.float16)
+    elif case == "zeros":
+        x = np.zeros((1, K), dtype=np.float16)
+    elif case == "signed_zero":
+        x = np.where(rng.random((1, K)) < 0.5, np.float16(0.0), np.float16(-0.0)).astype(np.float16)
+        x[:, ::7] = np.float16(3.0)
+    else:
+        x = inputs.activations_t3(K, 1, 66)
+    x = x.astype(np.float16)
+    for p in [(2000, 2000, 3000, 3000), (0, 0, 0, 10000), (10000, 0, 0, 0), (3333, 3333, 3334, 0)]:
+        _topk_fused_case(g, torch, L, x, g.grinqh_topk_counts(K, p))
+    for counts in ([K - 3, 1, 1, 1], [0, K - 2, 1, 1], [1, 1, 1, K - 3], [K - 511, 0, 511, 0]):
+        _topk_fused_case(g, torch, L, x, counts)
+
+
+def test_vmm_topk_fused_ties_across_threads(g, torch):
+    """Runs of equal magnitudes that straddle the per-thread key runs, with cuts
+    landing inside a run: the channel-order tie break decides the level map."""
+    K, N = 4096, 1024
+    L = Layer(g, torch, K, N, (0, 2, 4, 6, 8), cfg=67, tile_n=512)
+    x = inputs.activations_t3(K, 1, 67).astype(np.float16)
+    x[0, 1000:1100] = np.float16(7.5)
+    x[0, 3000:3050] = np.float16(-7.5)
+    x[0, 10:4000:13] = np.float16(2.25)
+    ax = np.abs(x[0].astype(np.float32))
+    n75, n225 = int((ax == 7.5).sum()), int((ax == 2.25).sum())
+    above75 = int((ax > 7.5).sum())
+    above225 = int((ax > 2.25).sum())
+    cases = [
+        [K - (above75 + 70), 0, 0, 0, above75 + 70],                       # cut inside the 7.5 run
+        [K - (above225 + 7), 0, 0, above225 + 7 - (above75 + 3), above75 + 3],
+        [K - (above75 + n75), 0, 0, 0, above75 + n75],                     # cut at the end of a run
+        [K - (above75 + 1), 0, 0, 0, above75 + 1],                         # first of a run
+    ]
+    for counts in cases:
+        assert sum(counts) == K and min(counts) >= 0, counts
+        _topk_fused_case(g, torch, L, x, counts)
+
+
 # ------------------------------------------------------- calibration ----
 @pytest.mark.parametrize("K", [128, 1152, 4096, 14336])
 def test_calibrate_matches_oracle(g, torch, K):
