@@ -84,7 +84,7 @@ enum { GRINQH_ASSIGN_THRESHOLD = 0, GRINQH_ASSIGN_TOPK = 1 };
 enum { GRINQH_VMM_ACCUMULATE = 1 };
 /* Options of grinqh_set_option, and the kernels GRINQH_OPT_VMM_KERNEL names. */
 enum { GRINQH_OPT_VMM_KERNEL = 1, GRINQH_OPT_GROUPS_PER_WG = 2, GRINQH_OPT_PREFILL_TILE = 3,
-       GRINQH_OPT_LUT_GROUPS = 4 };
+       GRINQH_OPT_LUT_GROUPS = 4, GRINQH_OPT_PREFILL_CUS = 5 };
 enum { GRINQH_KERNEL_AUTO = 0, GRINQH_KERNEL_PER_PLANE = 1, GRINQH_KERNEL_GENERAL = 2 };
 
 /* Infrastructure, not an operation of the paper.  Fill the auto fields
@@ -273,6 +273,8 @@ GRINQH_API int grinqh_vmm_lut_threshold(const grinqh_layer_desc* desc, const voi
  *     (kernels that take fewer use their maximum).
  *   GRINQH_OPT_PREFILL_TILE: 1, 2, 3 = 256x256, 256x128, 128x128 prefill tiles.
  *   GRINQH_OPT_LUT_GROUPS: 1..16 groups per workgroup of the LUT VMM.
+ *   GRINQH_OPT_PREFILL_CUS: 1..4096, the CU count the prefill balances its
+ *     rounds of 256x256 tiles for (0: the device's).
  * Returns GRINQH_EINVAL for an unknown option or a value out of range.  The
  * setting is read when a call enqueues its kernels; set it between calls. */
 GRINQH_API int grinqh_set_option(int option, int value);

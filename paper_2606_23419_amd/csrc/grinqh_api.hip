@@ -431,6 +431,7 @@ int grinqh_set_option(int opt, int value) {
     case GRINQH_OPT_GROUPS_PER_WG: field = &Options::groups_per_wg; hi = 4; break;
     case GRINQH_OPT_PREFILL_TILE: field = &Options::prefill_tile; hi = 3; break;
     case GRINQH_OPT_LUT_GROUPS: field = &Options::lut_groups; hi = 16; break;
+    case GRINQH_OPT_PREFILL_CUS: field = &Options::prefill_cus; hi = 4096; break;
     default: return fail(GRINQH_EINVAL, "option=%d is not a known option", opt);
   }
   if (value < lo || value > hi) return fail(GRINQH_EINVAL, "option %d: value %d outside %d..%d", opt, value, lo, hi);

@@ -79,6 +79,7 @@ struct Options {
   int groups_per_wg;    // groups of 128 channels per workgroup, where a kernel allows it
   int prefill_tile;     // 1..3: 256x256, 256x128, 128x128
   int lut_groups;       // groups per workgroup of the LUT VMM
+  int prefill_cus;      // CUs the prefill counts its rounds in (0: the device's)
 };
 int option(int Options::*field);
 

@@ -81,7 +81,7 @@ __global__ __launch_bounds__(kThreadsPF) void k_prefill(const uint8_t* __restric
                                                        const uint16_t* __restrict__ scales,
                                                        const uint16_t* __restrict__ x,
                                                        float* __restrict__ y, Layer L, int M,
-                                                       int accumulate, int2 win) {
+                                                       int accumulate, int2 win, int n_base) {
   constexpr int BM = 64 * MB, BN = 64 * NB;
   constexpr int XI = BM * kBK * 2 / 1024 / 4;      // X copy instructions per wave and step
   constexpr int WI = kBK * BN / 1024 / 4;          // code copy instructions per wave and step
@@ -117,7 +117,7 @@ __global__ __launch_bounds__(kThreadsPF) void k_prefill(const uint8_t* __restric
     rblk = win.x * wr + p / win.y;
     ctile = win.y * wc + p % win.y;
   }
-  const int m0 = rblk * BM, n0 = ctile * BN;
+  const int m0 = rblk * BM, n0 = n_base + ctile * BN;
   const int T = L.T, K = L.K, N = L.N;
   const int steps = K / kBK;                       // even: K is a multiple of 128
   const int tile = n0 / T, o0 = n0 - tile * T;     // BN divides T
@@ -321,10 +321,12 @@ __global__ __launch_bounds__(kThreadsPF) void k_prefill(const uint8_t* __restric
     }
 }
 
+// Output columns [n_begin, n_begin + n_cols) of Y; n_begin and n_cols are
+// multiples of the tile width.
 template <int U, int MB, int NB>
 void launch_cfg(const Layer& L, const void* codes, const void* scales, const void* x, int M,
-                float* y, int accumulate, hipStream_t s) {
-  const int gx = (M + 64 * MB - 1) / (64 * MB), gy = L.N / (64 * NB);
+                float* y, int accumulate, hipStream_t s, int n_begin, int n_cols) {
+  const int gx = (M + 64 * MB - 1) / (64 * MB), gy = n_cols / (64 * NB);
   // windows of up to 4 row blocks x 8 column tiles (about one XCD's worth of
   // workgroups at one per CU), the largest powers of two dividing the grid
   int2 win = make_int2(1, 1);
@@ -333,15 +335,28 @@ void launch_cfg(const Layer& L, const void* codes, const void* scales, const voi
   if (win.x == 1) win.y = 1;   // one row block: the plain order already shares X
   hipLaunchKernelGGL((k_prefill<U, MB, NB>), dim3((unsigned)(gx * gy)), dim3(kThreadsPF), 0, s,
                      (const uint8_t*)codes, (const uint16_t*)scales, (const uint16_t*)x, y, L, M,
-                     accumulate, win);
+                     accumulate, win, n_begin);
 }
 
 template <int U>
 void launch_u(int cfg, const Layer& L, const void* codes, const void* scales, const void* x, int M,
-              float* y, int accumulate, hipStream_t s) {
-  if (cfg == 0) launch_cfg<U, 4, 4>(L, codes, scales, x, M, y, accumulate, s);
-  else if (cfg == 1) launch_cfg<U, 4, 2>(L, codes, scales, x, M, y, accumulate, s);
-  else launch_cfg<U, 2, 2>(L, codes, scales, x, M, y, accumulate, s);
+              float* y, int accumulate, hipStream_t s, int n_begin, int n_cols) {
+  if (cfg == 0) launch_cfg<U, 4, 4>(L, codes, scales, x, M, y, accumulate, s, n_begin, n_cols);
+  else if (cfg == 1) launch_cfg<U, 4, 2>(L, codes, scales, x, M, y, accumulate, s, n_begin, n_cols);
+  else launch_cfg<U, 2, 2>(L, codes, scales, x, M, y, accumulate, s, n_begin, n_cols);
+}
+
+// Compute units of the current device (cached per device).
+int device_cus() {
+  static int cus[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (!cus[dev]) {
+    int v = 0;
+    if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || v <= 0) v = 256;
+    cus[dev] = v;
+  }
+  return cus[dev];
 }
 
 }  // namespace
@@ -350,13 +365,42 @@ void launch_u(int cfg, const Layer& L, const void* codes, const void* scales, co
 // (one resident per CU), else 256 x 128 on the same condition, else 128 x 128
 // (short prompts; two resident per CU).  GRINQH_OPT_PREFILL_TILE = 1
 // (256 x 256), 2 (256 x 128) or 3 (128 x 128) forces one.
+//
+// At 256 x 256 the workgroups run in rounds of one per CU.  When the tiles
+// leave a last round less than half full (e.g. 896 tiles on 256 CUs: three
+// rounds and a half), the launch is split by columns: whole rounds of
+// 256 x 256 tiles, then the remaining columns as 256 x 128 tiles, which fill
+// one round that takes about half as long.  GRINQH_OPT_PREFILL_CUS sets the
+// CU count the rounds are counted in (tests); 0 takes the device's.
 int launch_prefill(const Layer& L, const void* codes, const void* scales, const void* x, int M,
                    float* y, int accumulate, hipStream_t s) {
   const long mb256 = (M + 255) / 256;
   int cfg = mb256 * (L.N / 256) >= 160 ? 0 : mb256 * (L.N / 128) >= 160 ? 1 : 2;
-  if (const int v = option(&Options::prefill_tile)) cfg = v - 1;
-  if (L.u == 2) launch_u<2>(cfg, L, codes, scales, x, M, y, accumulate, s);
-  else launch_u<1>(cfg, L, codes, scales, x, M, y, accumulate, s);
+  int n_split = 0;   // columns of the 256 x 256 part when split
+  if (const int v = option(&Options::prefill_tile)) {
+    cfg = v - 1;
+  } else if (cfg == 0) {
+    const int o = option(&Options::prefill_cus);
+    const long cus = o ? o : device_cus();
+    const long gx = mb256, gy = L.N / 256, tiles = gx * gy;
+    if (tiles > cus && tiles % cus != 0) {
+      long c = gy - 1;
+      while (c > 0 && (c * gx) % cus != 0) --c;
+      if (c > 0 && 2 * (gy - c) * gx <= cus) n_split = (int)(256 * c);
+    }
+  }
+  auto go = [&](int cf, int nb, int nc) {
+    if (L.u == 2) launch_u<2>(cf, L, codes, scales, x, M, y, accumulate, s, nb, nc);
+    else launch_u<1>(cf, L, codes, scales, x, M, y, accumulate, s, nb, nc);
+  };
+  if (n_split) {
+    go(0, 0, n_split);
+    int st = check_launch("prefill");
+    if (st) return st;
+    go(1, n_split, L.N - n_split);
+  } else {
+    go(cfg, 0, L.N);
+  }
   return check_launch("prefill");
 }
 

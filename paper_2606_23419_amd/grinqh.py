@@ -29,6 +29,7 @@ GRINQH_OPT_VMM_KERNEL = 1
 GRINQH_OPT_GROUPS_PER_WG = 2
 GRINQH_OPT_PREFILL_TILE = 3
 GRINQH_OPT_LUT_GROUPS = 4
+GRINQH_OPT_PREFILL_CUS = 5
 GRINQH_KERNEL_AUTO = 0
 GRINQH_KERNEL_PER_PLANE = 1
 GRINQH_KERNEL_GENERAL = 2

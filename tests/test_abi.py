@@ -262,9 +262,11 @@ def test_set_option_validation(g):
     assert S(g.GRINQH_OPT_GROUPS_PER_WG, 5) == -1
     assert S(g.GRINQH_OPT_PREFILL_TILE, 4) == -1
     assert S(g.GRINQH_OPT_LUT_GROUPS, 17) == -1
+    assert S(g.GRINQH_OPT_PREFILL_CUS, 4097) == -1
     assert "outside" in g.grinqh_last_error()
     for opt, hi in [(g.GRINQH_OPT_VMM_KERNEL, 2), (g.GRINQH_OPT_GROUPS_PER_WG, 4),
-                    (g.GRINQH_OPT_PREFILL_TILE, 3), (g.GRINQH_OPT_LUT_GROUPS, 16)]:
+                    (g.GRINQH_OPT_PREFILL_TILE, 3), (g.GRINQH_OPT_LUT_GROUPS, 16),
+                    (g.GRINQH_OPT_PREFILL_CUS, 4096)]:
         assert S(opt, hi) == 0
         assert S(opt, 0) == 0          # back to the launchers' own choice
 

@@ -802,8 +802,30 @@ def test_prefill_rows_match_decode_at_top_level(g, torch):
 PREFILL_FULL = [  # name, K, N, levels, M
     ("qkv 4096->6144 M2048", 4096, 6144, inputs.LEVELS_B, 2048),
     ("gate_up 4096->28672 M512", 4096, 28672, inputs.LEVELS_B, 512),
+    ("gate_up 4096->28672 M2048 (split rounds)", 4096, 28672, inputs.LEVELS_B, 2048),
     ("down 14336->4096 M300", 14336, 4096, inputs.LEVELS_B, 300),
 ]
+
+
+@pytest.mark.parametrize("cus,K,N,levels,tile_n,M", [
+    (64, 128, 5120, (0, 2, 4, 8), 512, 2048),       # 160 tiles: 128 at 256x256, then 4 columns at 256x128
+    (64, 256, 5120, (0, 2, 3, 4, 8), 512, 1900),    # 1-bit planes, ragged last row block
+    (80, 128, 6144, (0, 2, 4, 6, 8), 1024, 1800)])  # 192 tiles: 160, then 4 columns
+def test_prefill_split_rounds(g, torch, opts, cus, K, N, levels, tile_n, M):
+    """A launch whose 256x256 tiles leave a part-filled last round runs whole
+    rounds at 256x256 and the remaining columns at 256x128."""
+    opts(g.GRINQH_OPT_PREFILL_CUS, cus)
+    L = Layer(g, torch, K, N, levels, cfg=68, tile_n=tile_n)
+    x = inputs.activations_t3(K, M, 68, 3)
+    y = g.grinqh_prefill(L.desc, L.pc, L.ps, _dev(torch, x))
+    torch.cuda.synchronize()
+    ref = orc.prefill(L.codes, L.scales, x)
+    assert rowwise(_host(y), ref) <= TOL
+    assert prefill_bound_ok(_host(y), L.codes, L.scales, x)
+    opts(g.GRINQH_OPT_PREFILL_CUS, 0)
+    y2 = g.grinqh_prefill(L.desc, L.pc, L.ps, _dev(torch, x))
+    torch.cuda.synchronize()
+    assert rowwise(_host(y2), _host(y)) <= 1e-6
 
 
 @pytest.mark.parametrize("name,K,N,levels,M", PREFILL_FULL, ids=[f[0] for f in PREFILL_FULL])
