@@ -106,7 +106,7 @@ __device__ __forceinline__ float double_offset_factor(int e) {
   return ((e >> 1) & 1) ? 0.0625f : 1.0f;
 }
 
-template <int LPR, int D>
+template <int LPR, int D, bool TOPK>
 __global__ __launch_bounds__(256) void k_vmm_sr(
     const uint8_t* __restrict__ codes, const uint16_t* __restrict__ scales,
     const uint16_t* __restrict__ x, const uint8_t* __restrict__ lm, float* __restrict__ y,
@@ -157,8 +157,10 @@ __global__ __launch_bounds__(256) void k_vmm_sr(
   if (lane < 12) (&s_empty[wave][0][0])[lane] = lane < 8 ? kNoRow : (kEmpty << 16);
 
   // top-k mode: the token's cuts from the whole x, the same in every workgroup
-  __shared__ __align__(16) topksel::Scratch s_tk;
-  if (fused == 2) topksel::select_cuts(x, L.K, tk, s_tk);
+  // (top-k kernels only: the others hold no selection scratch)
+  __shared__ __align__(16) uint8_t s_tk_raw[TOPK ? sizeof(topksel::Scratch) : 16];
+  topksel::Scratch& s_tk = *reinterpret_cast<topksel::Scratch*>(s_tk_raw);
+  if constexpr (TOPK) topksel::select_cuts(x, L.K, tk, s_tk);
 
   // ---- grade, sort into big and small rows, write this wave's lists
   const float fx = h2f((uint16_t)xv);
@@ -167,7 +169,7 @@ __global__ __launch_bounds__(256) void k_vmm_sr(
 #pragma unroll
   for (int j = 0; j < kMaxLevels - 1; ++j) graded += ax >= th.theta[j] ? 1 : 0;
   const int lvl = min(fused == 1 ? graded
-                      : fused == 2 ? topksel::level_of(xv, k, tk.n, s_tk)
+                      : TOPK ? topksel::level_of(xv, k, tk.n, s_tk)
                                    : (int)(lv & 0xFFu),
                       n_top);
   if (fused && lm_out && t == 0 && valid) lm_out[k] = (uint8_t)lvl;
@@ -347,7 +349,7 @@ __global__ __launch_bounds__(256) void k_vmm_sr(
 // waves' work and pads each list once per group rather than once per wave,
 // for two workgroup barriers in the prologue; it pays on launches of two
 // groups per workgroup, where each wave otherwise pads four lists.
-template <int LPR, int D>
+template <int LPR, int D, bool TOPK>
 __global__ __launch_bounds__(256) void k_vmm_sg(
     const uint8_t* __restrict__ codes, const uint16_t* __restrict__ scales,
     const uint16_t* __restrict__ x, const uint8_t* __restrict__ lm, float* __restrict__ y,
@@ -401,8 +403,10 @@ __global__ __launch_bounds__(256) void k_vmm_sg(
   if (wave == 0 && lane < ENT) E[EMPTY * ENT + lane] = (lane % 12) < 8 ? kNoRow : (kEmpty << 16);
 
   // top-k mode: the token's cuts from the whole x, the same in every workgroup
-  __shared__ __align__(16) topksel::Scratch s_tk;
-  if (fused == 2) topksel::select_cuts(x, L.K, tk, s_tk);
+  // (top-k kernels only: the others hold no selection scratch)
+  __shared__ __align__(16) uint8_t s_tk_raw[TOPK ? sizeof(topksel::Scratch) : 16];
+  topksel::Scratch& s_tk = *reinterpret_cast<topksel::Scratch*>(s_tk_raw);
+  if constexpr (TOPK) topksel::select_cuts(x, L.K, tk, s_tk);
 
   // ---- grade, sort into big and small rows
   const float fx = h2f((uint16_t)xv);
@@ -411,7 +415,7 @@ __global__ __launch_bounds__(256) void k_vmm_sg(
 #pragma unroll
   for (int j = 0; j < kMaxLevels - 1; ++j) graded += ax >= th.theta[j] ? 1 : 0;
   const int lvl = min(fused == 1 ? graded
-                      : fused == 2 ? topksel::level_of(xv, k, tk.n, s_tk)
+                      : TOPK ? topksel::level_of(xv, k, tk.n, s_tk)
                                    : (int)(lv & 0xFFu),
                       n_top);
   if (fused && lm_out && t == 0 && valid) lm_out[k] = (uint8_t)lvl;
@@ -619,12 +623,22 @@ void launch_sr(int gw, hipStream_t s, const void* codes, const void* scales, con
                const uint8_t* lm, float* y, const Layer& L, int fused, const Thresholds& th,
                const TopkCuts& tk, uint8_t* lm_out) {
   const dim3 grid((unsigned)(L.tiles * ((L.groups + gw - 1) / gw)));
-  if (gw == 2)
-    hipLaunchKernelGGL((k_vmm_sg<LPR, 4>), grid, dim3(256), 0, s,
+  // top-k selection is its own instantiation: the other kernels carry no
+  // selection code or scratch
+  if (gw == 2 && fused == 2)
+    hipLaunchKernelGGL((k_vmm_sg<LPR, 4, true>), grid, dim3(256), 0, s,
+                       (const uint8_t*)codes, (const uint16_t*)scales, (const uint16_t*)x, lm, y, L,
+                       gw, fused, th, tk, lm_out);
+  else if (gw == 2)
+    hipLaunchKernelGGL((k_vmm_sg<LPR, 4, false>), grid, dim3(256), 0, s,
+                       (const uint8_t*)codes, (const uint16_t*)scales, (const uint16_t*)x, lm, y, L,
+                       gw, fused, th, tk, lm_out);
+  else if (fused == 2)
+    hipLaunchKernelGGL((k_vmm_sr<LPR, 4, true>), grid, dim3(256), 0, s,
                        (const uint8_t*)codes, (const uint16_t*)scales, (const uint16_t*)x, lm, y, L,
                        gw, fused, th, tk, lm_out);
   else
-    hipLaunchKernelGGL((k_vmm_sr<LPR, 4>), grid, dim3(256), 0, s,
+    hipLaunchKernelGGL((k_vmm_sr<LPR, 4, false>), grid, dim3(256), 0, s,
                        (const uint8_t*)codes, (const uint16_t*)scales, (const uint16_t*)x, lm, y, L,
                        gw, fused, th, tk, lm_out);
 }
