@@ -32,6 +32,7 @@ namespace topksel {
 constexpr int kCutsMax = kMaxLevels - 1;
 constexpr int kThreads = 256;
 constexpr int kMaxK = 16384;   // channel indices fit the low 16 bits of a composite
+static_assert(kMaxK <= 65536, "a composite holds 65535 - k in 16 bits");
 
 struct Scratch {
   uint32_t hist1[256];
@@ -79,7 +80,7 @@ __device__ __forceinline__ uint32_t key_at(const uint4& v, int i) {
 }
 
 // Leaves the cuts in S.cut; ends with a workgroup barrier.  x: the token's
-// fp16 x [K], K a multiple of 128 and at most 16384, 16-byte aligned.
+// fp16 x [K], K a multiple of 128 and at most kMaxK, 16-byte aligned.
 __device__ __forceinline__ void select_cuts(const uint16_t* __restrict__ x, int K, const TopkCuts& tk,
                                             Scratch& S) {
   const int tid = threadIdx.x, lane = tid & 63;
