@@ -209,7 +209,10 @@ GRINQH_API int grinqh_vmm_threshold(const grinqh_layer_desc* desc, const void* p
  * Requires B = 1, K <= 16384, 2-bit planes with tile_n in {256, 512, 1024}
  * (GRINQH_EUNSUPPORTED otherwise: grinqh_assign + grinqh_vmm serve the
  * other cases) and x 16-byte aligned.  level_map_out, if not NULL, receives
- * the levels (uint8 [K]).  Other arguments as grinqh_vmm. */
+ * the levels (uint8 [K]).  Other arguments as grinqh_vmm.
+ * Every workgroup repeats the selection, so on Llama3-8B-sized layers this
+ * is slower than grinqh_assign (top-k) followed by grinqh_vmm; it serves
+ * callers that cannot keep a level map or launch the assignment apart. */
 GRINQH_API int grinqh_vmm_topk(const grinqh_layer_desc* desc, const void* packed_codes,
                                const void* packed_scales, const void* x, int32_t B,
                                const int32_t* counts, uint8_t* level_map_out, float* y,
