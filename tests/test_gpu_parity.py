@@ -329,6 +329,37 @@ def test_vmm_topk_fused_adversarial(g, torch, case):
         _topk_fused_case(g, torch, L, x, counts)
 
 
+@pytest.mark.parametrize("K,N,levels,tile_n", [
+    (640, 1024, (0, 2, 4, 6, 8), 256), (1152, 2048, (0, 2, 4, 8), 512), (4096, 2048, (0, 2, 4, 6, 8), 1024)])
+def test_vmm_topk_fused_shared_lists(g, torch, opts, K, N, levels, tile_n):
+    """The top-k selecting kernel with the workgroup-shared lists (two groups
+    per workgroup, as on the MLP projections)."""
+    opts(g.GRINQH_OPT_GROUPS_PER_WG, 2)
+    L = Layer(g, torch, K, N, levels, cfg=69, tile_n=tile_n)
+    x = inputs.activations_t3(K, 1, 69)
+    for p in inputs.BUDGETS[tuple(levels)].values():
+        _topk_fused_case(g, torch, L, x, g.grinqh_topk_counts(K, p))
+
+
+@pytest.mark.parametrize("name,K,N,xkind", [
+    ("gate|up 4096->28672 (shared lists)", 4096, 28672, "t3"),
+    ("down 14336->4096", 14336, 4096, "swiglu")])
+def test_vmm_topk_fused_full_size_every_output(g, torch, name, K, N, xkind):
+    """Every output of one fused top-k launch at a full MLP shape."""
+    levels = inputs.LEVELS_B
+    L = Layer(g, torch, K, N, levels, cfg=70, layer=K + N, codes_src=True)
+    x = (inputs.activations_swiglu if xkind == "swiglu" else inputs.activations_t3)(K, 1, 70, K + N)
+    counts = g.grinqh_topk_counts(K, inputs.BUDGETS[levels][4])
+    lm_out = torch.zeros((1, K), dtype=torch.uint8, device="cuda")
+    y = _host(g.grinqh_vmm_topk(L.desc, L.pc, L.ps, _dev(torch, x), counts, level_map_out=lm_out))
+    lm = orc.assign_topk(x, counts)
+    assert np.array_equal(_host(lm_out), lm), name
+    ref = oracle_all_outputs(L.codes, L.scales, x, lm, levels)
+    err = normwise(y, ref)
+    print(f"{name}: normwise {err:.2e}, elementwise {elementwise(y, ref):.2e}")
+    assert err <= TOL, (name, err)
+
+
 def test_vmm_topk_fused_ties_across_threads(g, torch):
     """Runs of equal magnitudes that straddle the per-thread key runs, with cuts
     landing inside a run: the channel-order tie break decides the level map."""
