@@ -4,9 +4,12 @@
 //   Y[m][n] = sum_k X[m][k] W_hat[n][k],  W_hat = s[k/128][n] (q[n][k] - 128),
 // a dense contraction, on the matrix cores (v_mfma_f32_32x32x16_f16).
 //
-// A workgroup of 4 waves computes a (64 MB) x (64 NB) tile of Y; each wave
-// owns a (32 MB) x (32 NB) quarter as MB x NB blocks of 32 x 32, so every
-// 16-byte operand fragment read from LDS feeds NB (or MB) MFMAs.  K advances
+// A workgroup of WV waves computes a (64 MB) x (64 NB) tile of Y; the waves
+// split it into RS row bands by WV / RS column bands, each wave's part as
+// blocks of 32 x 32, so every 16-byte operand fragment read from LDS feeds
+// several MFMAs.  The 256 x 256 tile runs 8 waves (two per SIMD, 128 x 64
+// each): one wave's unpack and LDS waits overlap the other's MFMAs, which a
+// single wave per SIMD (4 waves of 128 x 128) leaves idle.  K advances
 // 64 channels per step through two LDS buffers: while the waves multiply out
 // of one buffer they fill the other with the next step,
 //   - X: the [64 MB rows][64 k] fp16 tile, copied;
@@ -39,7 +42,6 @@ typedef _Float16 half2v __attribute__((ext_vector_type(2)));
 typedef float float16v __attribute__((ext_vector_type(16)));
 
 constexpr int kBK = 64;
-constexpr int kThreadsPF = 256;
 
 __device__ __forceinline__ uint32_t mul_half2(uint32_t a, uint32_t b) {
   return __builtin_bit_cast(uint32_t, __builtin_bit_cast(half2v, a) * __builtin_bit_cast(half2v, b));
@@ -76,21 +78,25 @@ struct WRegs {
   uint4 s[2];
 };
 
-template <int U, int MB, int NB>
-__global__ __launch_bounds__(kThreadsPF) void k_prefill(const uint8_t* __restrict__ codes,
+template <int U, int MB, int NB, int WV, int RS>
+__global__ __launch_bounds__(64 * WV) void k_prefill(const uint8_t* __restrict__ codes,
                                                        const uint16_t* __restrict__ scales,
                                                        const uint16_t* __restrict__ x,
                                                        float* __restrict__ y, Layer L, int M,
                                                        int accumulate, int2 win, int n_base) {
   constexpr int BM = 64 * MB, BN = 64 * NB;
-  constexpr int XI = BM * kBK * 2 / 1024 / 4;      // X copy instructions per wave and step
-  constexpr int WI = kBK * BN / 1024 / 4;          // code copy instructions per wave and step
+  constexpr int XI = BM * kBK * 2 / 1024 / WV;     // X copy instructions per wave and step
+  constexpr int WI = kBK * BN / 1024 / WV;         // code copy instructions per wave and step
   constexpr int RCH = BN / 16;                     // 16-byte chunks of one staged channel row
   constexpr int PPP = BN * U / 128;                // chunks per plane of a staged row
-  constexpr int CPT = BN / 64;                     // channels per thread and step
+  constexpr int CPT = kBK * BN / 16 / (64 * WV);   // channels per thread and step
   constexpr int NCG = kBK / CPT;                   // channel groups per step
   constexpr int kWords = 8 / U;                    // plane words per channel and 16 outputs
-  static_assert(CPT == 2 || CPT == 4, "tile width");
+  constexpr int MBW = 2 * MB / RS;                 // 32-row blocks per wave
+  constexpr int NBW = 2 * NB * RS / WV;            // 32-column blocks per wave
+  static_assert(WV == 4 || WV == 8, "waves");
+  static_assert(CPT == 2 || CPT == 4, "tile width for the waves");
+  static_assert(XI >= 1 && WI >= 1 && MBW >= 1 && NBW >= 1, "tile too small for the waves");
   // separate objects per buffer: the compiler then knows that a copy in
   // flight into one buffer does not alias reads of the other
   __shared__ __align__(16) _Float16 sX0[BM * kBK];
@@ -121,7 +127,7 @@ __global__ __launch_bounds__(kThreadsPF) void k_prefill(const uint8_t* __restric
   const int T = L.T, K = L.K, N = L.N;
   const int steps = K / kBK;                       // even: K is a multiple of 128
   const int tile = n0 / T, o0 = n0 - tile * T;     // BN divides T
-  const int wm = (wave >> 1) * 32 * MB, wn = (wave & 1) * 32 * NB;
+  const int wm = (wave / (WV / RS)) * 32 * MBW, wn = (wave % (WV / RS)) * 32 * NBW;
 
   // X copy: instruction i of this wave fills LDS rows 8 I .. 8 I + 7, I = 4 i +
   // wave, 16 bytes per lane; lane l takes the logical chunk that the swizzle
@@ -130,7 +136,7 @@ __global__ __launch_bounds__(kThreadsPF) void k_prefill(const uint8_t* __restric
   const uint16_t* xsrc[XI];
 #pragma unroll
   for (int i = 0; i < XI; ++i) {
-    const int row = 8 * (4 * i + wave) + (lane >> 3);
+    const int row = 8 * (WV * i + wave) + (lane >> 3);
     const int c = (lane & 7) ^ (row & 7) ^ ((row >> 3) & 1);
     xsrc[i] = x + (size_t)min(m0 + row, M - 1) * K + 8 * c;
   }
@@ -139,7 +145,7 @@ __global__ __launch_bounds__(kThreadsPF) void k_prefill(const uint8_t* __restric
     for (int i = 0; i < XI; ++i)
       __builtin_amdgcn_global_load_lds(
           (const __attribute__((address_space(1))) void*)(xsrc[i] + st * kBK),
-          (__attribute__((address_space(3))) void*)&sx[8 * kBK * (4 * i + wave)], 16, 0, 0);
+          (__attribute__((address_space(3))) void*)&sx[8 * kBK * (WV * i + wave)], 16, 0, 0);
   };
 
   // Code staging: the tile's part of a channel row is BN bytes at 8 bits
@@ -153,7 +159,7 @@ __global__ __launch_bounds__(kThreadsPF) void k_prefill(const uint8_t* __restric
   int wsrc[WI];
 #pragma unroll
   for (int i = 0; i < WI; ++i) {
-    const int q = 64 * (4 * i + wave) + lane;
+    const int q = 64 * (WV * i + wave) + lane;
     const int r = q / RCH, v = (q % RCH) ^ ((r / CPT) & 7);
     const int pl = v / PPP;
     wsrc[i] = r * L.RB + (pl < L.P ? pl : 0) * (T * U / 8) + 16 * (v % PPP);
@@ -164,7 +170,7 @@ __global__ __launch_bounds__(kThreadsPF) void k_prefill(const uint8_t* __restric
     for (int i = 0; i < WI; ++i)
       __builtin_amdgcn_global_load_lds(
           (const __attribute__((address_space(1))) void*)(base + wsrc[i]),
-          (__attribute__((address_space(3))) void*)&sp[1024 * (4 * i + wave)], 16, 0, 0);
+          (__attribute__((address_space(3))) void*)&sp[1024 * (WV * i + wave)], 16, 0, 0);
   };
 
   // W unpack: outputs 16 j .. 16 j + 15 of the tile, channels CPT cg .. of the step
@@ -238,11 +244,11 @@ __global__ __launch_bounds__(kThreadsPF) void k_prefill(const uint8_t* __restric
       }
   };
 
-  float16v acc[MB][NB];
+  float16v acc[MBW][NBW];
 #pragma unroll
-  for (int a = 0; a < MB; ++a)
+  for (int a = 0; a < MBW; ++a)
 #pragma unroll
-    for (int b = 0; b < NB; ++b) acc[a][b] = float16v{};
+    for (int b = 0; b < NBW; ++b) acc[a][b] = float16v{};
 
   // One step st: start the copies of X for st + 1 and of the codes for st + 2
   // (into the staging buffer that held st's codes) and the scale loads for
@@ -262,15 +268,15 @@ __global__ __launch_bounds__(kThreadsPF) void k_prefill(const uint8_t* __restric
     for (int ks = 0; ks < kBK / 16; ++ks) {
       if (ks % (4 / CPT) == 0) unpack(cur, ks / (4 / CPT), h[ks / (4 / CPT)]);
       const int c = 2 * ks + (lane >> 5);
-      half8 fa[MB], fb[NB];
+      half8 fa[MBW], fb[NBW];
 #pragma unroll
-      for (int a = 0; a < MB; ++a) fa[a] = *(const half8*)&xc[x_off(wm + 32 * a + (lane & 31), c)];
+      for (int a = 0; a < MBW; ++a) fa[a] = *(const half8*)&xc[x_off(wm + 32 * a + (lane & 31), c)];
 #pragma unroll
-      for (int b = 0; b < NB; ++b) fb[b] = *(const half8*)&wc[w_off(wn + 32 * b + (lane & 31), c)];
+      for (int b = 0; b < NBW; ++b) fb[b] = *(const half8*)&wc[w_off(wn + 32 * b + (lane & 31), c)];
 #pragma unroll
-      for (int a = 0; a < MB; ++a)
+      for (int a = 0; a < MBW; ++a)
 #pragma unroll
-        for (int b = 0; b < NB; ++b)
+        for (int b = 0; b < NBW; ++b)
           acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_f16(fa[a], fb[b], acc[a][b], 0, 0, 0);
       // one sub-step per scheduling region: the unpack spreads over the MFMAs
       if (ks + 1 < kBK / 16) __builtin_amdgcn_sched_barrier(0);
@@ -307,13 +313,13 @@ __global__ __launch_bounds__(kThreadsPF) void k_prefill(const uint8_t* __restric
   // element e of lane l of a 32 x 32 block: row 8 (e / 4) + 4 (l / 32) + e % 4,
   // column l % 32
 #pragma unroll
-  for (int a = 0; a < MB; ++a)
+  for (int a = 0; a < MBW; ++a)
 #pragma unroll
     for (int e = 0; e < 16; ++e) {
       const int m = m0 + wm + 32 * a + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
       if (m >= M) continue;
 #pragma unroll
-      for (int b = 0; b < NB; ++b) {
+      for (int b = 0; b < NBW; ++b) {
         float* dst = y + (size_t)m * N + n0 + wn + 32 * b + (lane & 31);
         const float v = acc[a][b][e] * L.sfac;   // 8-bit code units -> b_max units (exact)
         *dst = accumulate ? *dst + v : v;
@@ -323,7 +329,7 @@ __global__ __launch_bounds__(kThreadsPF) void k_prefill(const uint8_t* __restric
 
 // Output columns [n_begin, n_begin + n_cols) of Y; n_begin and n_cols are
 // multiples of the tile width.
-template <int U, int MB, int NB>
+template <int U, int MB, int NB, int WV, int RS>
 void launch_cfg(const Layer& L, const void* codes, const void* scales, const void* x, int M,
                 float* y, int accumulate, hipStream_t s, int n_begin, int n_cols) {
   const int gx = (M + 64 * MB - 1) / (64 * MB), gy = n_cols / (64 * NB);
@@ -333,7 +339,7 @@ void launch_cfg(const Layer& L, const void* codes, const void* scales, const voi
   while (win.x < 4 && gx % (2 * win.x) == 0) win.x *= 2;
   while (win.y < 8 && gy % (2 * win.y) == 0) win.y *= 2;
   if (win.x == 1) win.y = 1;   // one row block: the plain order already shares X
-  hipLaunchKernelGGL((k_prefill<U, MB, NB>), dim3((unsigned)(gx * gy)), dim3(kThreadsPF), 0, s,
+  hipLaunchKernelGGL((k_prefill<U, MB, NB, WV, RS>), dim3((unsigned)(gx * gy)), dim3(64 * WV), 0, s,
                      (const uint8_t*)codes, (const uint16_t*)scales, (const uint16_t*)x, y, L, M,
                      accumulate, win, n_begin);
 }
@@ -341,9 +347,14 @@ void launch_cfg(const Layer& L, const void* codes, const void* scales, const voi
 template <int U>
 void launch_u(int cfg, const Layer& L, const void* codes, const void* scales, const void* x, int M,
               float* y, int accumulate, hipStream_t s, int n_begin, int n_cols) {
-  if (cfg == 0) launch_cfg<U, 4, 4>(L, codes, scales, x, M, y, accumulate, s, n_begin, n_cols);
-  else if (cfg == 1) launch_cfg<U, 4, 2>(L, codes, scales, x, M, y, accumulate, s, n_begin, n_cols);
-  else launch_cfg<U, 2, 2>(L, codes, scales, x, M, y, accumulate, s, n_begin, n_cols);
+  // 256 x 256: 8 waves of 128 x 64 for 2-bit planes (gate_up at 2048 tokens
+  // 909 -> 939, qkv 755 -> 824 TFLOP/s); the 1-bit unpack needs more
+  // registers than two waves per SIMD leave, so 4 waves of 128 x 128 there.
+  // 256 x 128 and 128 x 128: 4 waves (8 waves of 64 x 64 read more LDS per
+  // MFMA and were no faster).
+  if (cfg == 0) launch_cfg<U, 4, 4, U == 2 ? 8 : 4, 2>(L, codes, scales, x, M, y, accumulate, s, n_begin, n_cols);
+  else if (cfg == 1) launch_cfg<U, 4, 2, 4, 2>(L, codes, scales, x, M, y, accumulate, s, n_begin, n_cols);
+  else launch_cfg<U, 2, 2, 4, 2>(L, codes, scales, x, M, y, accumulate, s, n_begin, n_cols);
 }
 
 // Compute units of the current device (cached per device).
