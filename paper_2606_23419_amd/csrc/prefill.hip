@@ -97,6 +97,9 @@ __global__ __launch_bounds__(64 * WV) void k_prefill(const uint8_t* __restrict__
   static_assert(WV == 4 || WV == 8, "waves");
   static_assert(CPT == 2 || CPT == 4, "tile width for the waves");
   static_assert(XI >= 1 && WI >= 1 && MBW >= 1 && NBW >= 1, "tile too small for the waves");
+  // every thread unpacks one (channel group, 16 outputs) unit and loads its
+  // scales: a thread without a unit would read scales past the tile
+  static_assert(NCG * (BN / 16) == 64 * WV, "threads and unpack units");
   // separate objects per buffer: the compiler then knows that a copy in
   // flight into one buffer does not alias reads of the other
   __shared__ __align__(16) _Float16 sX0[BM * kBK];
