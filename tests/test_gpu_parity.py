@@ -588,6 +588,75 @@ def test_decode_layers_graph_replays_match_oracle(g, torch):
                 assert err <= TOL, (rep, li, name, err)
 
 
+def test_topk_and_prefill_graph_replays(g, torch, opts):
+    # The top-k paths (selection inside the VMM, and assignment launch + VMM)
+    # on a merged q|k|v and a down projection at 4 bits, and a prefill on the
+    # 8-wave 256 x 256 tile, captured as one HIP graph and replayed three
+    # times with eager work between: level maps bit-exact with the oracle's
+    # top-k on every replay, outputs within the tolerance of the oracle, and
+    # the prefill (fixed summation order) equal bit for bit to its eager run.
+    levels = inputs.LEVELS_B
+    p = inputs.BUDGETS[levels][4]
+    shapes = [("qkv", 4096, 6144, inputs.activations_t3), ("down", 14336, 4096, inputs.activations_swiglu)]
+    L = {name: Layer(g, torch, K, N, levels, cfg=81, layer=li, codes_src=True)
+         for li, (name, K, N, _) in enumerate(shapes)}
+    xs = {name: gen(K, 1, 81, li) for li, (name, K, _, gen) in enumerate(shapes)}
+    counts = {name: g.grinqh_topk_counts(K, p) for name, K, _, _ in shapes}
+    xd = {name: _dev(torch, v) for name, v in xs.items()}
+    y_f = {name: torch.zeros((1, N), dtype=torch.float32, device="cuda") for name, _, N, _ in shapes}
+    y_2 = {name: torch.zeros((1, N), dtype=torch.float32, device="cuda") for name, _, N, _ in shapes}
+    lm_f = {name: torch.full((1, K), 255, dtype=torch.uint8, device="cuda") for name, K, _, _ in shapes}
+    lm_2 = {name: torch.full((1, K), 255, dtype=torch.uint8, device="cuda") for name, K, _, _ in shapes}
+    opts(g.GRINQH_OPT_PREFILL_TILE, 1)              # 256 x 256, 8 waves
+    Kp, Np, M = 384, 1024, 300
+    Lp = Layer(g, torch, Kp, Np, (0, 2, 4, 8), cfg=82, layer=1)
+    xp = inputs.activations_t3(Kp, M, 82, 1)
+    xpd = _dev(torch, xp)
+    yp = torch.zeros((M, Np), dtype=torch.float32, device="cuda")
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+
+    def step():
+        for name, _, _, _ in shapes:
+            y_f[name].zero_()
+            g.grinqh_vmm_topk(L[name].desc, L[name].pc, L[name].ps, xd[name], counts[name],
+                              y=y_f[name], level_map_out=lm_f[name], accumulate=True)
+            g.grinqh_assign(L[name].desc, xd[name], g.GRINQH_ASSIGN_TOPK, counts=counts[name],
+                            out=lm_2[name])
+            g.grinqh_vmm(L[name].desc, L[name].pc, L[name].ps, xd[name], lm_2[name], y=y_2[name])
+        g.grinqh_prefill(Lp.desc, Lp.pc, Lp.ps, xpd, y=yp)
+
+    with torch.cuda.stream(s):
+        step()
+    torch.cuda.synchronize()
+    yp_eager = _host(yp).copy()
+    assert normwise(yp_eager, orc.prefill(Lp.codes, Lp.scales, xp)) <= TOL
+    lms, refs = {}, {}
+    for name, _, _, _ in shapes:
+        lms[name] = orc.assign_topk(xs[name], counts[name])
+        refs[name] = oracle_all_outputs(L[name].codes, L[name].scales, xs[name], lms[name], levels)
+    gr = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(gr, stream=s):
+        step()
+    for rep in range(3):
+        for name, _, _, _ in shapes:                # eager work between replays
+            y_f[name].fill_(float("nan"))
+            y_2[name].fill_(float("nan"))
+            lm_f[name].fill_(255)
+            lm_2[name].fill_(255)
+        yp.fill_(float("nan"))
+        torch.cuda.synchronize()
+        with torch.cuda.stream(s):
+            gr.replay()
+        torch.cuda.synchronize()
+        for name, _, _, _ in shapes:
+            assert np.array_equal(_host(lm_f[name]), lms[name]), (rep, name, "fused")
+            assert np.array_equal(_host(lm_2[name]), lms[name]), (rep, name, "assignment launch")
+            assert normwise(_host(y_f[name]), refs[name]) <= TOL, (rep, name, "fused")
+            assert normwise(_host(y_2[name]), refs[name]) <= TOL, (rep, name, "assignment launch")
+        assert np.array_equal(_host(yp).view(np.uint32), yp_eager.view(np.uint32)), rep
+
+
 @pytest.mark.parametrize("kernel", ["pp", "dot2"])
 @pytest.mark.parametrize("gw", ["1", "2", "3", "4"])
 @pytest.mark.parametrize("tile_n", [256, 512, 1024])
