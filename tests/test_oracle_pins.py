@@ -206,6 +206,16 @@ def test_vmm_all_skipped_is_zero():
     assert np.all(y == 0.0)
 
 
+def test_reconstruct_at_zero_bits_is_zero():
+    # R2: a skipped channel contributes exactly 0.  (A 0-bit read has q_b = 0
+    # and phi = 2^(b_max-1), so s * phi cancels z = -2^(b_max-1) s exactly:
+    # the formula and the skip agree bit for bit.)
+    q = np.arange(256, dtype=np.uint8)
+    s = np.full(256, 0.0123, dtype=np.float64)
+    for b_max in (4, 6, 8):
+        assert np.all(orc.reconstruct(q >> (8 - b_max), s, 0, b_max) == 0.0)
+
+
 def test_vmm_single_level_equals_truncated_uniform_quantiser():
     # all channels at b bits: the layer acts as a uniform b-bit quantiser whose
     # grid is the 8-bit grid coarsened by 2^(8-b), offset by phi.
