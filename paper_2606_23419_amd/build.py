@@ -23,8 +23,12 @@ HIPCC_FLAGS = [
 
 # per-source extra flags: prefill.hip keeps its fixed-size register arrays in
 # registers (the compiler would otherwise place some in LDS, which its
-# double-buffered tiles need)
-SOURCE_FLAGS = {"prefill.hip": ["-mllvm", "-disable-promote-alloca-to-lds"]}
+# double-buffered tiles need); vmm_pp.hip preloads its first kernel arguments
+SOURCE_FLAGS = {"prefill.hip": ["-mllvm", "-disable-promote-alloca-to-lds"],
+                # the batch-1 kernels' leading arguments (x, level map, groups)
+                # arrive in scalar registers at wave launch, so the first load
+                # of x does not wait for a kernel-argument load
+                "vmm_pp.hip": ["-mllvm", "-amdgpu-kernarg-preload-count=16"]}
 
 
 def hipcc() -> str:

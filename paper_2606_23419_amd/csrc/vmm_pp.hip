@@ -108,9 +108,9 @@ __device__ __forceinline__ float double_offset_factor(int e) {
 
 template <int LPR, int D, bool TOPK>
 __global__ __launch_bounds__(256) void k_vmm_sr(
-    const uint8_t* __restrict__ codes, const uint16_t* __restrict__ scales,
-    const uint16_t* __restrict__ x, const uint8_t* __restrict__ lm, float* __restrict__ y,
-    Layer L, int gw, int fused, Thresholds th, TopkCuts tk, uint8_t* __restrict__ lm_out) {
+    const uint16_t* __restrict__ x, const uint8_t* __restrict__ lm, int gw, int groups, int fused,
+    const uint8_t* __restrict__ codes, const uint16_t* __restrict__ scales, float* __restrict__ y,
+    Layer L, Thresholds th, TopkCuts tk, uint8_t* __restrict__ lm_out) {
   constexpr int T = LPR * 16;            // outputs of the tile
   constexpr int PLANE = T / 4;           // bytes of one plane row
   constexpr int NLG = 64 / LPR;          // lane groups per wave
@@ -131,22 +131,25 @@ __global__ __launch_bounds__(256) void k_vmm_sr(
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int half = lane >> 5, hl = lane & 31;
-  const int t = blockIdx.x % L.tiles;
-  const int g0 = (blockIdx.x / L.tiles) * gw;
-  const int ng = min(gw, L.groups - g0);
-  const int lg = lane / LPR, li = lane % LPR;
-  const int n_top = L.n_levels - 1;
-  const __amdgpu_buffer_rsrc_t rsrc = tile_rsrc(codes + (size_t)t * L.K * L.RB, L);
-  const uint32_t li4 = (uint32_t)li * 4u;
-
-  // ---- loads first: x and the level map of this lane's row (lanes 0-31 the
-  // first group, 32-63 the second), the scales of this lane's 16 outputs for
-  // both groups (a group past the last reads the last one again, from cache)
+  const int t = blockIdx.x;
+  const int g0 = blockIdx.y * gw;
+  const int ng = min(gw, groups - g0);
+  // loads first: x and the level map of this lane's row (lanes 0-31 the
+  // first group, 32-63 the second).  They need no field of L, so they go
+  // out before the wave waits for the layer's scalars (x, lm, gw, groups and
+  // fused lead the argument list and arrive preloaded in scalar registers)
   const int gg = half;
   const bool valid = gg < ng;
   const int k = (g0 + min(gg, ng - 1)) * kGroup + 32 * wave + hl;
   const uint32_t xv = x[k];
   const uint32_t lv = (fused ? (const uint8_t*)x : lm)[k];   // ignored when graded here
+  const int lg = lane / LPR, li = lane % LPR;
+  const int n_top = L.n_levels - 1;
+  const __amdgpu_buffer_rsrc_t rsrc = tile_rsrc(codes + (size_t)t * L.K * L.RB, L);
+  const uint32_t li4 = (uint32_t)li * 4u;
+
+  // the scales of this lane's 16 outputs for both groups (a group past the
+  // last reads the last one again, from cache)
   uint4 scw[MAXG][2];
 #pragma unroll
   for (int g = 0; g < MAXG; ++g) {
@@ -351,9 +354,9 @@ __global__ __launch_bounds__(256) void k_vmm_sr(
 // groups per workgroup, where each wave otherwise pads four lists.
 template <int LPR, int D, bool TOPK>
 __global__ __launch_bounds__(256) void k_vmm_sg(
-    const uint8_t* __restrict__ codes, const uint16_t* __restrict__ scales,
-    const uint16_t* __restrict__ x, const uint8_t* __restrict__ lm, float* __restrict__ y,
-    Layer L, int gw, int fused, Thresholds th, TopkCuts tk, uint8_t* __restrict__ lm_out) {
+    const uint16_t* __restrict__ x, const uint8_t* __restrict__ lm, int gw, int groups, int fused,
+    const uint8_t* __restrict__ codes, const uint16_t* __restrict__ scales, float* __restrict__ y,
+    Layer L, Thresholds th, TopkCuts tk, uint8_t* __restrict__ lm_out) {
   constexpr int T = LPR * 16;            // outputs of the tile
   constexpr int PLANE = T / 4;           // bytes of one plane row
   constexpr int NLG = 64 / LPR;          // lane groups per wave
@@ -376,22 +379,25 @@ __global__ __launch_bounds__(256) void k_vmm_sg(
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int half = lane >> 5, hl = lane & 31;
-  const int t = blockIdx.x % L.tiles;
-  const int g0 = (blockIdx.x / L.tiles) * gw;
-  const int ng = min(gw, L.groups - g0);
-  const int lg = lane / LPR, li = lane % LPR;
-  const int n_top = L.n_levels - 1;
-  const __amdgpu_buffer_rsrc_t rsrc = tile_rsrc(codes + (size_t)t * L.K * L.RB, L);
-  const uint32_t li4 = (uint32_t)li * 4u;
-
-  // ---- loads first: x and the level map of this lane's row (lanes 0-31 the
-  // first group, 32-63 the second), the scales of this lane's 16 outputs for
-  // both groups (a group past the last reads the last one again, from cache)
+  const int t = blockIdx.x;
+  const int g0 = blockIdx.y * gw;
+  const int ng = min(gw, groups - g0);
+  // loads first: x and the level map of this lane's row (lanes 0-31 the
+  // first group, 32-63 the second).  They need no field of L, so they go
+  // out before the wave waits for the layer's scalars (x, lm, gw, groups and
+  // fused lead the argument list and arrive preloaded in scalar registers)
   const int gg = half;
   const bool valid = gg < ng;
   const int k = (g0 + min(gg, ng - 1)) * kGroup + 32 * wave + hl;
   const uint32_t xv = x[k];
   const uint32_t lv = (fused ? (const uint8_t*)x : lm)[k];   // ignored when graded here
+  const int lg = lane / LPR, li = lane % LPR;
+  const int n_top = L.n_levels - 1;
+  const __amdgpu_buffer_rsrc_t rsrc = tile_rsrc(codes + (size_t)t * L.K * L.RB, L);
+  const uint32_t li4 = (uint32_t)li * 4u;
+
+  // the scales of this lane's 16 outputs for both groups (a group past the
+  // last reads the last one again, from cache)
   uint4 scw[MAXG][2];
 #pragma unroll
   for (int g = 0; g < MAXG; ++g) {
@@ -622,25 +628,25 @@ template <int LPR>
 void launch_sr(int gw, hipStream_t s, const void* codes, const void* scales, const void* x,
                const uint8_t* lm, float* y, const Layer& L, int fused, const Thresholds& th,
                const TopkCuts& tk, uint8_t* lm_out) {
-  const dim3 grid((unsigned)(L.tiles * ((L.groups + gw - 1) / gw)));
+  const dim3 grid((unsigned)L.tiles, (unsigned)((L.groups + gw - 1) / gw));
   // top-k selection is its own instantiation: the other kernels carry no
   // selection code or scratch
   if (gw == 2 && fused == 2)
     hipLaunchKernelGGL((k_vmm_sg<LPR, 4, true>), grid, dim3(256), 0, s,
-                       (const uint8_t*)codes, (const uint16_t*)scales, (const uint16_t*)x, lm, y, L,
-                       gw, fused, th, tk, lm_out);
+                       (const uint16_t*)x, lm, gw, L.groups, fused, (const uint8_t*)codes,
+                       (const uint16_t*)scales, y, L, th, tk, lm_out);
   else if (gw == 2)
     hipLaunchKernelGGL((k_vmm_sg<LPR, 4, false>), grid, dim3(256), 0, s,
-                       (const uint8_t*)codes, (const uint16_t*)scales, (const uint16_t*)x, lm, y, L,
-                       gw, fused, th, tk, lm_out);
+                       (const uint16_t*)x, lm, gw, L.groups, fused, (const uint8_t*)codes,
+                       (const uint16_t*)scales, y, L, th, tk, lm_out);
   else if (fused == 2)
     hipLaunchKernelGGL((k_vmm_sr<LPR, 4, true>), grid, dim3(256), 0, s,
-                       (const uint8_t*)codes, (const uint16_t*)scales, (const uint16_t*)x, lm, y, L,
-                       gw, fused, th, tk, lm_out);
+                       (const uint16_t*)x, lm, gw, L.groups, fused, (const uint8_t*)codes,
+                       (const uint16_t*)scales, y, L, th, tk, lm_out);
   else
     hipLaunchKernelGGL((k_vmm_sr<LPR, 4, false>), grid, dim3(256), 0, s,
-                       (const uint8_t*)codes, (const uint16_t*)scales, (const uint16_t*)x, lm, y, L,
-                       gw, fused, th, tk, lm_out);
+                       (const uint16_t*)x, lm, gw, L.groups, fused, (const uint8_t*)codes,
+                       (const uint16_t*)scales, y, L, th, tk, lm_out);
 }
 
 }  // namespace
