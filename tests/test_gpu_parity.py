@@ -526,6 +526,38 @@ def test_full_size_every_output(g, torch, name, K, N, levels, xkind, B):
     assert err <= TOL, (name, err)
 
 
+def test_large_k_every_path(g, torch):
+    # K = 98304 (768 groups): channel indices past 16 bits and tiles of
+    # 48 MB, through the fused threshold VMM (level map written out), the
+    # standalone assignment + level-map VMM, two tokens (union depth) and a
+    # prefill; every output against the oracle, computed a block of outputs
+    # at a time.  Thresholds come from the oracle's calibration (the GPU
+    # calibration takes K <= 16384).
+    K, N, levels = 98304, 1024, inputs.LEVELS_B
+    L = Layer(g, torch, K, N, levels, cfg=83, layer=1, tile_n=512, codes_src=True)
+    x = inputs.activations_t3(K, 2, 83, 1)
+    calib = inputs.activations_t3(K, 8, 84, 1)
+    th = orc.calibrate_thresholds([np.abs(r.astype(np.float64)) for r in calib], inputs.BUDGETS[levels][4])
+    xd = _dev(torch, x)
+    lm_out = torch.zeros((1, K), dtype=torch.uint8, device="cuda")
+    y1 = _host(g.grinqh_vmm_threshold(L.desc, L.pc, L.ps, xd[:1], th, level_map_out=lm_out))
+    lm = orc.assign_threshold(x, th)
+    assert np.array_equal(_host(lm_out), lm[:1])
+    lm2 = g.grinqh_assign(L.desc, xd, g.GRINQH_ASSIGN_THRESHOLD, thresholds=th)
+    assert np.array_equal(_host(lm2), lm)
+    y2 = _host(g.grinqh_vmm(L.desc, L.pc, L.ps, xd[:1], lm2[:1]))
+    yb = _host(g.grinqh_vmm(L.desc, L.pc, L.ps, xd, lm2))           # B = 2, union depth
+    ref = oracle_all_outputs(L.codes, L.scales, x, lm, levels, chunk=256)
+    assert normwise(y1, ref[:1]) <= TOL
+    assert normwise(y2, ref[:1]) <= TOL
+    assert normwise(yb, ref) <= TOL
+    xp = inputs.activations_t3(K, 3, 85, 1)
+    yp = _host(g.grinqh_prefill(L.desc, L.pc, L.ps, _dev(torch, xp)))
+    refp = np.concatenate([orc.prefill(L.codes[n:n + 256], L.scales[:, n:n + 256], xp)
+                           for n in range(0, N, 256)], axis=1)
+    assert normwise(yp, refp) <= TOL
+
+
 def test_decode_layers_graph_replays_match_oracle(g, torch):
     # Two layers of the decode step (merged q|k|v, o, merged gate|up, down at
     # 4 bits, thresholds calibrated per input, grading fused) captured as one
