@@ -558,6 +558,29 @@ def test_large_k_every_path(g, torch):
     assert normwise(yp, refp) <= TOL
 
 
+@pytest.mark.parametrize("tile_n", [512, 1024])
+def test_large_n_every_path(g, torch, tile_n):
+    # N = 131072 (128 or 256 tiles in one launch) over two groups, through the
+    # same paths; every output against the oracle
+    K, N, levels = 256, 131072, inputs.LEVELS_B
+    L = Layer(g, torch, K, N, levels, cfg=86, layer=tile_n, tile_n=tile_n, codes_src=True)
+    x = inputs.activations_t3(K, 2, 86, tile_n)
+    calib = inputs.activations_t3(K, 16, 87, tile_n)
+    th = _host(g.grinqh_calibrate(L.desc, _dev(torch, calib), inputs.BUDGETS[levels][4]))
+    xd = _dev(torch, x)
+    lm = orc.assign_threshold(x, th)
+    y1 = _host(g.grinqh_vmm_threshold(L.desc, L.pc, L.ps, xd[:1], th))
+    lm2 = g.grinqh_assign(L.desc, xd, g.GRINQH_ASSIGN_THRESHOLD, thresholds=th)
+    assert np.array_equal(_host(lm2), lm)
+    yb = _host(g.grinqh_vmm(L.desc, L.pc, L.ps, xd, lm2))
+    ref = oracle_all_outputs(L.codes, L.scales, x, lm, levels, chunk=16384)
+    assert normwise(y1, ref[:1]) <= TOL
+    assert normwise(yb, ref) <= TOL
+    xp = inputs.activations_t3(K, 5, 88, tile_n)
+    yp = _host(g.grinqh_prefill(L.desc, L.pc, L.ps, _dev(torch, xp)))
+    assert normwise(yp, orc.prefill(L.codes, L.scales, xp)) <= TOL
+
+
 def test_decode_layers_graph_replays_match_oracle(g, torch):
     # Two layers of the decode step (merged q|k|v, o, merged gate|up, down at
     # 4 bits, thresholds calibrated per input, grading fused) captured as one
