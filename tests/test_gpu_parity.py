@@ -923,7 +923,10 @@ def test_prefill_codes_source_all_code_values(g, torch):
     assert prefill_bound_ok(y, L.codes, L.scales, x)
 
 
-def test_prefill_accumulate_and_reproducible(g, torch):
+@pytest.mark.parametrize("tile", [0, 1, 2, 3])   # automatic, then each tile forced
+def test_prefill_accumulate_and_reproducible(g, torch, tile, opts):
+    if tile:
+        opts(g.GRINQH_OPT_PREFILL_TILE, tile)
     K, N, M = 384, 512, 150
     L = Layer(g, torch, K, N, (0, 2, 4, 8), cfg=62, layer=2)
     x = inputs.activations_t3(K, M, 62, 2)
