@@ -181,9 +181,11 @@ GRINQH_API int grinqh_assign(const grinqh_layer_desc* desc, int mode, const void
  *   and each token uses its own prefix of it.
  *   x: fp16 [B][K]; level_map: uint8 [B][K], values < n_levels (a larger
  *   value is read as the top level); y: fp32 [B][N]; 1 <= B <= 4.
- *   flags: 0 -> y is overwritten; GRINQH_VMM_ACCUMULATE -> y += result (the
- *   caller initialised y).  Accumulation order across K is not fixed, so y
- *   is reproducible to rounding, not bit for bit.  Any other flag bit is
+ *   flags: 0 -> y is overwritten (cleared by one extra launch before the
+ *   VMM, whose workgroups add their partial sums into y); GRINQH_VMM_ACCUMULATE
+ *   -> y += result (the caller initialised y, e.g. once for many VMMs into
+ *   one buffer).  Accumulation order across K is not fixed, so y is
+ *   reproducible to rounding, not bit for bit.  Any other flag bit is
  *   GRINQH_EINVAL. */
 GRINQH_API int grinqh_vmm(const grinqh_layer_desc* desc, const void* packed_codes,
                const void* packed_scales, const void* x, const uint8_t* level_map,
