@@ -3,7 +3,8 @@
 wrong sign of the offset, the wrong RTN divisor or rounding, the count
 rounding, a wrong prefix shift, no quantile interpolation, scales of the
 wrong output, a transposed prefill operand, a LUT read without nesting, a
-wrong calibration mean, the sign bit kept in the magnitude key) is planted
+wrong calibration mean, the sign bit kept in the magnitude key, the planes,
+fields or rows of the packed layout in another order) is planted
 in a copy of the oracle, and the pin tests run against the copy must fail.
 
 CPU only; the GPU library is not involved.
@@ -42,6 +43,12 @@ MUTATIONS = {
     "calibration mean": ("    return (acc / np.float64(count)).astype(np.float32)",
                          "    return (acc / np.float64(count + 1)).astype(np.float32)"),
     "sign bit kept in the magnitude key": ("    return bits & 0x7FFF\n", "    return bits\n"),
+    "planes least significant first": ("                    field = (q >> (b_max - j * u)) & mask",
+                                       "                    field = (q >> ((j - 1) * u)) & mask"),
+    "fields in reversed output order": ("                    bit = o * u\n",
+                                        "                    bit = (tile_n - 1 - o) * u\n"),
+    "rows channel-major across tiles": ("            row = (t * K + k) * R\n",
+                                        "            row = (k * (N // tile_n) + t) * R\n"),
 }
 
 
