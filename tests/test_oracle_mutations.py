@@ -13,6 +13,8 @@ import os
 import shutil
 import subprocess
 import sys
+import tempfile
+from concurrent.futures import ThreadPoolExecutor
 
 import pytest
 
@@ -52,30 +54,48 @@ MUTATIONS = {
 }
 
 
-def _run_pins(tmp_path, mutation=None):
-    for d in ("oracle", "tests", "synth"):
-        shutil.copytree(os.path.join(ROOT, d), tmp_path / d,
-                        ignore=shutil.ignore_patterns("__pycache__", "*.so", "test_oracle_mutations.py"))
-    if mutation is not None:
-        old, new = mutation
-        path = tmp_path / "oracle" / "grinqh_oracle.py"
-        src = path.read_text()
-        assert src.count(old) == 1, "mutation site not found exactly once"
-        path.write_text(src.replace(old, new))
-    return subprocess.run([sys.executable, "-m", "pytest", *PINS, "-q", "-x", "-m", "not gpu",
-                           "-p", "no:cacheprovider"], cwd=tmp_path, capture_output=True, text=True,
-                          timeout=600)
+def _run_pins(mutation=None):
+    """Copy the oracle, tests and inputs to a fresh directory, plant the
+    mutation (if any) and run the pin tests there; returns the run."""
+    with tempfile.TemporaryDirectory() as tmp:
+        for d in ("oracle", "tests", "synth"):
+            shutil.copytree(os.path.join(ROOT, d), os.path.join(tmp, d),
+                            ignore=shutil.ignore_patterns("__pycache__", "*.so", "test_oracle_mutations.py"))
+        if mutation is not None:
+            old, new = mutation
+            path = os.path.join(tmp, "oracle", "grinqh_oracle.py")
+            with open(path) as f:
+                src = f.read()
+            assert src.count(old) == 1, "mutation site not found exactly once"
+            with open(path, "w") as f:
+                f.write(src.replace(old, new))
+        return subprocess.run([sys.executable, "-m", "pytest", *PINS, "-q", "-x", "-m", "not gpu",
+                               "-p", "no:cacheprovider"], cwd=tmp, capture_output=True, text=True,
+                              timeout=600)
 
 
-def test_unmutated_copy_passes(tmp_path):
+_RESULTS = {}
+
+
+def _results():
+    # every run at once, a few in parallel (each is an independent process)
+    if not _RESULTS:
+        names = [None] + sorted(MUTATIONS)
+        with ThreadPoolExecutor(max_workers=min(5, os.cpu_count() or 1)) as ex:
+            runs = list(ex.map(lambda n: _run_pins(MUTATIONS.get(n)), names))
+        _RESULTS.update(zip(names, runs))
+    return _RESULTS
+
+
+def test_unmutated_copy_passes():
     # the control: the copied tree runs the pins cleanly, so a failure below
     # comes from the planted mistake and not from the copy
-    r = _run_pins(tmp_path)
+    r = _results()[None]
     assert r.returncode == 0, r.stdout[-800:]
 
 
 @pytest.mark.parametrize("name", sorted(MUTATIONS))
-def test_pins_catch_planted_mistake(name, tmp_path):
-    r = _run_pins(tmp_path, MUTATIONS[name])
+def test_pins_catch_planted_mistake(name):
+    r = _results()[name]
     assert r.returncode == 1, f"no pin failed for: {name}\n{r.stdout[-400:]}"   # 1: tests failed
     assert " failed" in r.stdout, r.stdout[-400:]
