@@ -503,6 +503,8 @@ EVERY = [
     ("per-plane B=2 qkv 4096->6144", 4096, 6144, inputs.LEVELS_B, "t3", 2),
     ("per-plane B=4 down 14336->4096", 14336, 4096, inputs.LEVELS_B, "swiglu", 4),
     ("1-bit planes qkv 4096->6144", 4096, 6144, inputs.LEVELS_C, "t3", 1),
+    ("b_max 6 batch1 gate|up 4096->28672", 4096, 28672, (0, 2, 4, 6), "t3", 1),
+    ("b_max 4 batch1 down 14336->4096", 14336, 4096, (0, 2, 4), "swiglu", 1),
 ]
 
 
